@@ -1,0 +1,136 @@
+"""Verification-time estimator (Sec. 4.4) and its fitting procedure (App. C).
+
+The batch verification latency is modelled as an additive combination of linear
+work, attention interactions and cached-token reads:
+
+    T_hat = a * N_linear + b_compute * N_interactions + b_read * N_cached + c
+
+with, for a batch of requests that each bring L_new,i new tokens on top of
+L_cached,i cached ones (L_total,i = L_cached,i + L_new,i):
+
+    N_linear = sum_i L_new,i,   N_interactions = sum_i L_total,i * L_new,i,
+    N_cached = sum_i L_cached,i.
+
+For the verification step, L_new,i = gamma_i + 1 (the drafts plus the row of the
+last committed token) and L_cached,i = ctx_len_i.  The coefficients are fitted by
+ordinary least squares; App. C reports a train/test split, 1000-sample bootstrap
+95% confidence intervals and 5-fold cross-validation, all provided here.  Fitting is
+host-side, offline work in fp64; the fitted model is what an SLO-aware scheduler
+queries for each candidate batch.
+"""
+from __future__ import annotations
+
+import json
+from dataclasses import dataclass, asdict
+
+import numpy as np
+
+FEATURES = ("N_linear", "N_interactions", "N_cached")
+
+
+def step_features(ctx_len, gamma) -> np.ndarray:
+    """[N_linear, N_interactions, N_cached] of one verification batch (Sec. 4.4)."""
+    ctx = np.asarray(ctx_len, dtype=np.float64)
+    new = np.asarray(gamma, dtype=np.float64) + 1.0
+    return np.array([new.sum(), ((ctx + new) * new).sum(), ctx.sum()])
+
+
+@dataclass
+class LatencyModel:
+    a: float
+    b_compute: float
+    b_read: float
+    c: float
+    ci: dict | None = None
+
+    @property
+    def coef(self) -> np.ndarray:
+        return np.array([self.a, self.b_compute, self.b_read, self.c])
+
+    def predict(self, X) -> np.ndarray:
+        X = np.atleast_2d(np.asarray(X, dtype=np.float64))
+        return X @ self.coef[:3] + self.c
+
+    def predict_batch(self, ctx_len, gamma) -> float:
+        return float(self.predict(step_features(ctx_len, gamma))[0])
+
+    def to_json(self) -> str:
+        return json.dumps(asdict(self), indent=1)
+
+    @staticmethod
+    def from_json(s: str) -> "LatencyModel":
+        return LatencyModel(**json.loads(s))
+
+
+def _design(X) -> np.ndarray:
+    X = np.atleast_2d(np.asarray(X, dtype=np.float64))
+    return np.hstack([X, np.ones((X.shape[0], 1))])
+
+
+def fit_ols(X, y) -> LatencyModel:
+    """Least squares through the normal equations (A^T A) w = A^T y, A = [X | 1].
+
+    Columns are scaled to unit norm before solving so that features spanning many
+    orders of magnitude (N_interactions vs N_linear) stay well conditioned."""
+    A = _design(X)
+    y = np.asarray(y, dtype=np.float64)
+    s = np.linalg.norm(A, axis=0)
+    s[s == 0] = 1.0
+    As = A / s
+    w = np.linalg.solve(As.T @ As, As.T @ y) / s
+    return LatencyModel(*[float(v) for v in w])
+
+
+def metrics(y, yhat, n_features: int = 3) -> dict:
+    y = np.asarray(y, dtype=np.float64)
+    yhat = np.asarray(yhat, dtype=np.float64)
+    r = y - yhat
+    ss_res = float((r ** 2).sum())
+    ss_tot = float(((y - y.mean()) ** 2).sum())
+    n = y.shape[0]
+    r2 = 1.0 - ss_res / ss_tot if ss_tot > 0 else float("nan")
+    adj = 1.0 - (1.0 - r2) * (n - 1) / (n - n_features - 1) if n > n_features + 1 else float("nan")
+    return {"r2": r2, "adj_r2": adj, "rmse": float(np.sqrt(ss_res / n)), "mae": float(np.abs(r).mean()),
+            "mape_pct": float(100.0 * np.abs(r / y).mean()), "max_err": float(np.abs(r).max())}
+
+
+def bootstrap_ci(X, y, n_boot: int = 1000, level: float = 0.95, seed: int = 0) -> dict:
+    """Percentile bootstrap confidence intervals of the four coefficients."""
+    X = np.atleast_2d(np.asarray(X, dtype=np.float64))
+    y = np.asarray(y, dtype=np.float64)
+    rng = np.random.default_rng(seed)
+    n = y.shape[0]
+    W = np.empty((n_boot, 4))
+    for b in range(n_boot):
+        idx = rng.integers(0, n, size=n)
+        W[b] = fit_ols(X[idx], y[idx]).coef
+    lo, hi = (1 - level) / 2 * 100, (1 + level) / 2 * 100
+    names = ("a", "b_compute", "b_read", "c")
+    return {nm: (float(np.percentile(W[:, k], lo)), float(np.percentile(W[:, k], hi)))
+            for k, nm in enumerate(names)}
+
+
+def kfold_r2(X, y, k: int = 5, seed: int = 0) -> np.ndarray:
+    X = np.atleast_2d(np.asarray(X, dtype=np.float64))
+    y = np.asarray(y, dtype=np.float64)
+    idx = np.random.default_rng(seed).permutation(y.shape[0])
+    folds = np.array_split(idx, k)
+    out = []
+    for f in range(k):
+        te = folds[f]
+        tr = np.concatenate([folds[g] for g in range(k) if g != f])
+        m = fit_ols(X[tr], y[tr])
+        out.append(metrics(y[te], m.predict(X[te]))["r2"])
+    return np.array(out)
+
+
+def fit_report(X_train, y_train, X_test, y_test, n_boot: int = 1000, seed: int = 0) -> dict:
+    """The App. C protocol: OLS on the training split, bootstrap CIs, 5-fold CV on the
+    training split, accuracy metrics on both splits."""
+    m = fit_ols(X_train, y_train)
+    m.ci = bootstrap_ci(X_train, y_train, n_boot, seed=seed)
+    cv = kfold_r2(X_train, y_train, 5, seed)
+    return {"model": asdict(m),
+            "train": metrics(y_train, m.predict(X_train)),
+            "test": metrics(y_test, m.predict(X_test)),
+            "cv_r2_mean": float(cv.mean()), "cv_r2_std": float(cv.std())}
