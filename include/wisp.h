@@ -1,0 +1,195 @@
+/*
+ * wisp.h -- C ABI of the MI355X (gfx950) batched speculative-verification step.
+ *
+ * The step is the server-side verification of WISP (arXiv 2601.11652): Sec. 4.5
+ * ("batched one-step verification") forwards each request's drafted block on top of
+ * its cached prefix KV in one pass, then applies the speculative-sampling rule of
+ * Sec. 2.4 (Eq. (1) acceptance u <= min(1, p/q), Eq. (2) first rejection R and
+ * accepted length L = R - 1, Eq. (3) the extra token), returning (L, extra token)
+ * per request.  At a rejection the extra token is drawn from norm(max(0, p - q)) --
+ * the residual that makes the rule lossless (Leviathan et al., cited in Sec. 4.5);
+ * after a fully accepted block it is drawn from p.
+ *
+ * Conventions for every entry point:
+ *   - "DEVICE" pointers are HIP device memory owned by the caller; "HOST" pointers
+ *     are ordinary host memory owned by the caller and read during the call only.
+ *   - All GPU work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
+ *     the default stream).  Calls return after enqueueing; outputs are valid once
+ *     the stream is synchronised.  Nothing here allocates device memory except
+ *     where stated; scratch comes from the caller's workspace.
+ *   - Non-zero return values are errors; wisp_last_error() returns a thread-local
+ *     message for the last failing call.  No C++ exception crosses this boundary.
+ *   - Calls that share a workspace must not overlap on the GPU.
+ */
+#ifndef WISP_H
+#define WISP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WISP_OK = 0,
+  WISP_E_INVALID = -1,      /* bad descriptor, NULL pointer, gamma > 16, ctx_len < 0, T < 0   */
+  WISP_E_CAPACITY = -2,     /* page table too short for ctx_len + gamma + 1 tokens           */
+  WISP_E_WORKSPACE = -3,    /* workspace smaller than wisp_workspace_size()                  */
+  WISP_E_UNSUPPORTED = -4,  /* shape outside what the kernels implement                      */
+  WISP_E_HIP = -5,          /* HIP runtime error                                             */
+  WISP_E_DEVICE_INPUT = -6  /* a device-side input check failed (token id, block id)         */
+} wisp_status;
+
+typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
+
+#define WISP_PAGE 16        /* tokens per KV page                                            */
+#define WISP_GAMMA_MAX 16   /* most draft tokens per request                                 */
+
+/*
+ * Decoder-only transformer (RMSNorm, rotary embedding with rotate-half pairing,
+ * grouped-query attention, SwiGLU MLP, untied LM head) -- the target model of the
+ * verification engine (Sec. 4.5).  The paper names its target models (Qwen3,
+ * Llama) but not their internals; this layout follows the Llama-3 family.
+ *
+ * All weight pointers are DEVICE pointers of `dtype`.  The per-layer arrays are
+ * HOST arrays of n_layers DEVICE pointers.
+ *   embed       [vocab][d_model]                 natural row-major
+ *   final_norm, attn_norm[l], mlp_norm[l]  [d_model]
+ *   w_qkv[l]    rows (n_q + 2 n_kv) * head_dim  (W_q rows, then W_k, then W_v), K = d_model
+ *   w_o[l]      rows d_model,   K = n_q * head_dim
+ *   w_gate_up[l] rows 2 * d_ff (W_gate rows, then W_up), K = d_model
+ *   w_down[l]   rows d_model,   K = d_ff
+ *   lm_head     rows vocab,     K = d_model
+ * Linear weights ("rows x K", nn.Linear's [out][in]) must be stored in the packed
+ * form made by wisp_pack_linear(): for WISP_BF16 an MFMA-fragment order, for
+ * WISP_F32 plain row-major.
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rms_eps;      /* RMSNorm epsilon (1e-5 for the Llama shapes)                       */
+  float rope_base;    /* rotary base theta                                                 */
+  int32_t dtype;      /* wisp_dtype of weights, KV pages and GEMM-input activations        */
+  const void *embed, *final_norm, *lm_head;
+  const void *const *attn_norm, *const *w_qkv, *const *w_o;
+  const void *const *mlp_norm, *const *w_gate_up, *const *w_down;
+} wisp_model;
+
+/*
+ * Paged KV cache (PageAttention-style fixed-size blocks plus a per-request block
+ * table, Sec. 4.5).  Two DEVICE pools of `dtype`, each
+ *   [n_layers][n_blocks][n_kv_heads][page of 16 * head_dim elements].
+ * Inside one page (one block, one kv head) element (slot s, dim e) sits at
+ *   K:  ((e / 32) * 4 + (e % 32) / 8) * 128 + s * 8 + e % 8
+ *   V:  ((e / 16) * 4 + s / 4) * 64 + (e % 16) * 4 + s % 4
+ * (the operand order of gfx950's 16x16x32 matrix instructions, so one page streams
+ * as contiguous 1 KiB wave loads).  head_dim must be a multiple of 32.
+ * Token t of request i lives in block kv_page_table[i][t / 16], slot t % 16.
+ */
+typedef struct {
+  void *k_pool;
+  void *v_pool;
+  int32_t n_blocks;
+  int32_t page_size;  /* must be WISP_PAGE                                                 */
+} wisp_kv;
+
+/*
+ * One verification batch (a micro-batch chosen by the scheduler, Sec. 4.3).
+ * Request i brings gamma[i] draft tokens on top of ctx_len[i] cached tokens; the
+ * step forwards gamma[i] + 1 rows [root, y_1..y_gamma] at positions
+ * ctx_len[i] .. ctx_len[i] + gamma[i], where root is the last committed token
+ * (the previous round's extra token), whose KV is not cached yet.  Row j's logits
+ * score draft y_{j+1}; row gamma[i] is the bonus position.
+ */
+typedef struct {
+  int32_t B;
+  const int32_t *ctx_len;        /* HOST [B]  tokens already cached, >= 0                   */
+  const int32_t *gamma;          /* HOST [B]  0..WISP_GAMMA_MAX; 0 = ordinary decoding      */
+  const uint32_t *req_id;        /* HOST [B]  keys the request's random stream; NULL = i    */
+  const int32_t *kv_page_table;  /* DEVICE [B][pt_stride] block ids                         */
+  int32_t pt_stride;             /* pages per request in the table                         */
+  float temperature;             /* target temperature: > 0 sampled, 0 greedy              */
+} wisp_batch_desc;
+
+/* Bytes of DEVICE workspace wisp_verify needs for this model and batch (0 on error). */
+size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc);
+
+/*
+ * Pack one linear weight (natural [rows][cols] row-major, DEVICE `src`) into the
+ * layout the GEMMs read (DEVICE `dst`, same byte size; must not alias src).
+ * WISP_BF16: rows % 32 == 0 and cols % 16 == 0; the packed matrix is a sequence of
+ * 32 x 16 fragments, fragment (rb, kb) at ((rb * cols/16 + kb) * 512) elements,
+ * lane l's 8 elements at l * 8 holding row rb*32 + l%32, columns kb*16 + (l/32)*8 + 0..7.
+ * Row blocks are independent, so several matrices stacked by rows (W_q|W_k|W_v)
+ * are packed by calling this once per matrix at dst + (row offset * cols).
+ * WISP_F32: a plain copy.
+ */
+wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t cols, int32_t dtype,
+                             void *stream);
+
+/*
+ * The verification step (Sec. 4.5): forward + acceptance, returns L and the extra token.
+ *   tokens        DEVICE int32 [M], M = sum(gamma+1): per request root, y_1..y_gamma
+ *   draft_probs   DEVICE fp32 [sum gamma][vocab]: q_j rows, request-major (finite, >= 0)
+ *   rng_seed      keys every random draw (Philox4x32-10, Salmon et al. SC'11): the
+ *                 acceptance draw of draft j uses counter (0, j, req_id, 1), word 0; the
+ *                 race over token k on logits row r uses counter (k/4, r, req_id, 2), word
+ *                 k%4; key = (lo32, hi32) of rng_seed; a word w maps to the uniform
+ *                 (2 * (w >> 9) + 1) * 2^-24 in (0, 1).  Vary the seed between rounds.
+ *   accept_len    DEVICE int32 [B]: L_i = R_i - 1 (Eq. (2))
+ *   out_tokens    DEVICE int32 [M]: request i's slots hold y_1..y_L, the extra token, then -1
+ *   target_logits DEVICE fp32 [M][vocab]: the target's logits of every row (required)
+ *   workspace     DEVICE scratch of >= wisp_workspace_size() bytes
+ * KV: K/V of all gamma+1 new positions are written in place (rejected drafts
+ * included); the valid prefix afterwards is ctx_len + 1 + L and later calls overwrite
+ * the stale slots (rollback by length).  Repeating a call with the same inputs gives
+ * the same outputs.  Extra tokens are drawn by an exponential race (Gumbel-max):
+ * argmax_k [score_k - ln(-ln u_k)], ties to the smallest k, score = ln(residual) after
+ * a rejection (or z = logits/T when the residual is empty), z after full acceptance.
+ * Device-side input faults (token id outside [0, vocab), block id outside
+ * [0, n_blocks)) are recorded in the workspace and reported by wisp_check().
+ */
+wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                        const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
+                        int32_t *accept_len, int32_t *out_tokens, float *target_logits,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The acceptance stage alone (Sec. 2.4, Eq. (1)-(3) with the residual), on given
+ * logits: the same kernels and random streams as wisp_verify's last stage.
+ * Uses desc->B, gamma, req_id, temperature only.  logits DEVICE fp32 [M][vocab].
+ */
+size_t wisp_accept_workspace_size(const wisp_batch_desc *desc);
+wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float *logits,
+                        const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
+                        int32_t *accept_len, int32_t *out_tokens, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/*
+ * The attention of the step on its own, for one layer's pools (the causal attention
+ * of the new rows over each request's paged KV inside Sec. 4.5's forward):
+ *   q   DEVICE [M][n_q_heads][head_dim] of model->dtype (already rotated)
+ *   out DEVICE [M][n_q_heads][head_dim] of model->dtype
+ * kv->k_pool / v_pool point at that layer's [n_blocks] pages.  Row j of request i sees
+ * keys 0 .. ctx_len[i] + j.  Workspace: wisp_workspace_size() of the same batch.
+ */
+wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                           const void *q, void *out, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* Uniform draws of the step's random stream: out[k] = draw (seed, req_id, tag, row, k),
+ * k < n (DEVICE fp32).  tag 1 = acceptance, 2 = race. */
+wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint32_t row, uint32_t n,
+                         float *out, void *stream);
+
+/* Synchronise `stream`, then report (and clear) device-side input faults recorded in
+ * `workspace` by the last wisp_verify / wisp_accept on it. */
+wisp_status wisp_check(void *workspace, void *stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *wisp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WISP_H */

@@ -199,8 +199,8 @@ def plain_decode(logits_row, temperature: float, seed: int, req_id: int, row: in
 # forward (Sec. 4.5)
 # ------------------------------------------------------------------------------------
 def paged_attention(q, k_pool, v_pool, page_table, ctx_len, n_new, n_kv: int, bf16: bool):
-    """q [M][n_q][hd] float64; pools of ONE layer (K [blocks][n_kv][16][hd], V
-    [blocks][n_kv][hd][16]) as float32 or bf16 bits (uint16).  Returns [M][n_q][hd] fp64."""
+    """q [M][n_q][hd] float64; pools of ONE layer ([blocks][n_kv][16*hd] pages in the
+    documented K / V page layouts) as float32 or bf16 bits (uint16).  Returns [M][n_q][hd] fp64."""
     q = _c(q, np.float64)
     M, n_q, hd = q.shape
     out = np.empty_like(q)
@@ -272,9 +272,9 @@ class OracleModel:
 
 
 def forward(model: OracleModel, k_pool, v_pool, page_table, ctx_len, n_new, tokens) -> np.ndarray:
-    """Forward the new rows; updates the host pools in place (numpy arrays laid out
-    [n_layers][n_blocks][n_kv][16][hd] for K and [n_layers][n_blocks][n_kv][hd][16] for V,
-    float32 or uint16 bf16 bits).  Returns fp32 logits [M][V]."""
+    """Forward the new rows; updates the host pools in place (numpy arrays
+    [n_layers][n_blocks][n_kv][16*hd] in the documented page layouts, float32 or uint16
+    bf16 bits).  Returns fp32 logits [M][V]."""
     assert k_pool.flags["C_CONTIGUOUS"] and v_pool.flags["C_CONTIGUOUS"]
     n_blocks = k_pool.shape[1]
     pt = _c(page_table, np.int32)

@@ -24,8 +24,8 @@ def host_model(shape: wi.ModelShape, seed: int = wi.MASTER_SEED) -> OracleModel:
 
 def empty_pools(shape: wi.ModelShape, n_blocks: int):
     dt = np.float32 if shape.dtype == "f32" else np.uint16
-    k = np.zeros((shape.n_layers, n_blocks, shape.n_kv_heads, wi.PAGE, shape.head_dim), dtype=dt)
-    v = np.zeros((shape.n_layers, n_blocks, shape.n_kv_heads, shape.head_dim, wi.PAGE), dtype=dt)
+    k = np.zeros((shape.n_layers, n_blocks, shape.n_kv_heads, wi.PAGE * shape.head_dim), dtype=dt)
+    v = np.zeros((shape.n_layers, n_blocks, shape.n_kv_heads, wi.PAGE * shape.head_dim), dtype=dt)
     return k, v
 
 
@@ -50,11 +50,14 @@ def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=Non
             K, V = wi.kv_values(mix.seed, l, i, 0, n, s.n_kv_heads, s.head_dim, "cpu", dt)
             Kn = _to_storage(K, s)
             Vn = _to_storage(V, s)
+            kidx = wi.k_page_index(s.head_dim)
+            vidx = wi.v_page_index(s.head_dim)
             for t0 in range(0, n, wi.PAGE):
                 t1 = min(n, t0 + wi.PAGE)
                 blk = page_table[i, t0 // wi.PAGE]
-                kp[li, blk, :, : t1 - t0, :] = Kn[t0:t1].transpose(1, 0, 2)
-                vp[li, blk, :, :, : t1 - t0] = Vn[t0:t1].transpose(1, 2, 0)
+                sl = np.arange(t1 - t0)
+                kp[li, blk][:, kidx[sl]] = Kn[t0:t1].transpose(1, 0, 2)
+                vp[li, blk][:, vidx[sl]] = Vn[t0:t1].transpose(1, 0, 2)
 
 
 def prefill_context(model: OracleModel, mix: wi.Mix, pools, page_table, requests=None):

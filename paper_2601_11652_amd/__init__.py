@@ -1,0 +1,303 @@
+"""MI355X (gfx950) batched speculative-verification step of WISP (arXiv 2601.11652).
+
+Thin ctypes binding of ``libwisp.so`` (C ABI in include/wisp.h).  Every step of the
+verification path runs in the library's HIP kernels; this module only marshals
+arguments (torch tensors supply device memory and the stream).  Any call raises if
+the library has not been built -- there is no fallback implementation.
+
+Entry points keep the C names: wisp_verify, wisp_accept, wisp_attention,
+wisp_pack_linear, wisp_workspace_size, wisp_accept_workspace_size, wisp_uniform,
+wisp_check, wisp_last_error.  ``GpuModel`` and ``make_desc`` assemble the C structs.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwisp.so")
+
+WISP_OK = 0
+WISP_E_INVALID = -1
+WISP_E_CAPACITY = -2
+WISP_E_WORKSPACE = -3
+WISP_E_UNSUPPORTED = -4
+WISP_E_HIP = -5
+WISP_E_DEVICE_INPUT = -6
+WISP_F32 = 0
+WISP_BF16 = 1
+PAGE = 16
+GAMMA_MAX = 16
+TAG_ACCEPT = 1
+TAG_RACE = 2
+
+EXPORTS = ("wisp_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
+           "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_last_error")
+
+
+class WispError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"wisp status {status}: {msg}")
+        self.status = status
+
+
+_VP = C.c_void_p
+_PVP = C.POINTER(C.c_void_p)
+
+
+class wisp_model(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ff", C.c_int32),
+                ("vocab", C.c_int32), ("rms_eps", C.c_float), ("rope_base", C.c_float),
+                ("dtype", C.c_int32), ("embed", _VP), ("final_norm", _VP), ("lm_head", _VP),
+                ("attn_norm", _PVP), ("w_qkv", _PVP), ("w_o", _PVP), ("mlp_norm", _PVP),
+                ("w_gate_up", _PVP), ("w_down", _PVP)]
+
+
+class wisp_kv(C.Structure):
+    _fields_ = [("k_pool", _VP), ("v_pool", _VP), ("n_blocks", C.c_int32), ("page_size", C.c_int32)]
+
+
+class wisp_batch_desc(C.Structure):
+    _fields_ = [("B", C.c_int32), ("ctx_len", C.POINTER(C.c_int32)), ("gamma", C.POINTER(C.c_int32)),
+                ("req_id", C.POINTER(C.c_uint32)), ("kv_page_table", _VP), ("pt_stride", C.c_int32),
+                ("temperature", C.c_float)]
+
+
+_lib = None
+
+
+def load_library():
+    """The loaded libwisp.so (raises ImportError when it has not been built)."""
+    global _lib
+    if _lib is None:
+        _lib = _load()
+    return _lib
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with paper_2601_11652_amd.build.build() "
+                          "(or __graft_entry__.build()); there is no fallback path")
+    L = C.CDLL(LIB_PATH)
+    L.wisp_workspace_size.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_batch_desc)]
+    L.wisp_workspace_size.restype = C.c_size_t
+    L.wisp_accept_workspace_size.argtypes = [C.POINTER(wisp_batch_desc)]
+    L.wisp_accept_workspace_size.restype = C.c_size_t
+    L.wisp_pack_linear.argtypes = [_VP, _VP, C.c_int32, C.c_int32, C.c_int32, _VP]
+    L.wisp_verify.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
+                              _VP, _VP, C.c_uint64, _VP, _VP, _VP, _VP, C.c_size_t, _VP]
+    L.wisp_accept.argtypes = [C.POINTER(wisp_batch_desc), C.c_int32, _VP, _VP, _VP, C.c_uint64, _VP,
+                              _VP, _VP, C.c_size_t, _VP]
+    L.wisp_attention.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
+                                 _VP, _VP, _VP, C.c_size_t, _VP]
+    L.wisp_uniform.argtypes = [C.c_uint64, C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint32, _VP, _VP]
+    L.wisp_check.argtypes = [_VP, _VP]
+    L.wisp_last_error.argtypes = []
+    L.wisp_last_error.restype = C.c_char_p
+    for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
+                 "wisp_check"):
+        getattr(L, name).restype = C.c_int
+    return L
+
+
+class _Lazy:
+    def __getattr__(self, name):
+        return getattr(load_library(), name)
+
+
+lib = _Lazy()
+
+
+def wisp_last_error() -> str:
+    return lib.wisp_last_error().decode()
+
+
+def _ok(status: int):
+    if status != WISP_OK:
+        raise WispError(status, wisp_last_error())
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+# ------------------------------------------------------------------------------------------
+# struct builders
+# ------------------------------------------------------------------------------------------
+class BatchDesc:
+    """Owns the host arrays behind a wisp_batch_desc."""
+
+    def __init__(self, ctx_len, gamma, page_table=None, temperature: float = 1.0, req_id=None):
+        self.ctx_len = np.ascontiguousarray(ctx_len, dtype=np.int32)
+        self.gamma = np.ascontiguousarray(gamma, dtype=np.int32)
+        self.req_id = None if req_id is None else np.ascontiguousarray(req_id, dtype=np.uint32)
+        self.page_table = page_table          # torch int32 [B][stride] on the device
+        B = self.ctx_len.shape[0]
+        self.c = wisp_batch_desc()
+        self.c.B = B
+        self.c.ctx_len = self.ctx_len.ctypes.data_as(C.POINTER(C.c_int32))
+        self.c.gamma = self.gamma.ctypes.data_as(C.POINTER(C.c_int32))
+        self.c.req_id = (self.req_id.ctypes.data_as(C.POINTER(C.c_uint32))
+                         if self.req_id is not None else None)
+        if page_table is not None:
+            assert page_table.dtype.__str__() == "torch.int32" and page_table.is_contiguous()
+            self.c.kv_page_table = page_table.data_ptr()
+            self.c.pt_stride = page_table.shape[1]
+        self.c.temperature = float(temperature)
+
+    @property
+    def B(self):
+        return int(self.c.B)
+
+    @property
+    def M(self):
+        return int((self.gamma.astype(np.int64) + 1).sum())
+
+    @property
+    def S(self):
+        return int(self.gamma.sum())
+
+
+class KVPool:
+    """Two device pools [n_layers][n_blocks][n_kv][16 * head_dim] in the page layout."""
+
+    def __init__(self, k, v):
+        assert k.shape == v.shape and k.is_contiguous() and v.is_contiguous()
+        self.k, self.v = k, v
+        self.c = wisp_kv(k.data_ptr(), v.data_ptr(), k.shape[1], PAGE)
+
+    @staticmethod
+    def zeros(n_layers, n_blocks, n_kv, head_dim, dtype, device="cuda"):
+        import torch
+        shp = (n_layers, n_blocks, n_kv, PAGE * head_dim)
+        return KVPool(torch.zeros(shp, dtype=dtype, device=device), torch.zeros(shp, dtype=dtype, device=device))
+
+    def layer(self, l: int) -> "KVPool":
+        return KVPool(self.k[l:l + 1], self.v[l:l + 1])
+
+
+class GpuModel:
+    """Packed device weights plus the wisp_model struct pointing at them.
+
+    ``layer_source(l)`` returns the natural-layout device tensors of layer l (keys wq, wk,
+    wv, wo, w_gate, w_up, w_down, attn_norm, mlp_norm); ``glob`` holds embed, lm_head,
+    final_norm.  Natural tensors are released after packing."""
+
+    def __init__(self, shape, layer_source, glob, stream=None):
+        import torch
+        self.shape = shape
+        s = shape
+        dt = torch.float32 if s.dtype == "f32" else torch.bfloat16
+        code = WISP_F32 if s.dtype == "f32" else WISP_BF16
+        self.dtype_code = code
+        st = _stream(stream)
+        dev = glob["embed"].device
+
+        def pack(dst, src, rows, cols, row0=0):
+            assert src.is_contiguous() and src.dtype == dt and tuple(src.shape) == (rows, cols)
+            _ok(lib.wisp_pack_linear(dst.data_ptr() + row0 * cols * dst.element_size(), src.data_ptr(),
+                                     rows, cols, code, st))
+
+        self.layers = []
+        for l in range(s.n_layers):
+            w = layer_source(l)
+            qd, kd = s.n_q_heads * s.head_dim, s.n_kv_heads * s.head_dim
+            qkv = torch.empty((qd + 2 * kd) * s.d_model, dtype=dt, device=dev)
+            pack(qkv, w["wq"], qd, s.d_model, 0)
+            pack(qkv, w["wk"], kd, s.d_model, qd)
+            pack(qkv, w["wv"], kd, s.d_model, qd + kd)
+            wo = torch.empty(s.d_model * qd, dtype=dt, device=dev)
+            pack(wo, w["wo"], s.d_model, qd)
+            gu = torch.empty(2 * s.d_ff * s.d_model, dtype=dt, device=dev)
+            pack(gu, w["w_gate"], s.d_ff, s.d_model, 0)
+            pack(gu, w["w_up"], s.d_ff, s.d_model, s.d_ff)
+            wd = torch.empty(s.d_model * s.d_ff, dtype=dt, device=dev)
+            pack(wd, w["w_down"], s.d_model, s.d_ff)
+            self.layers.append({"attn_norm": w["attn_norm"].contiguous(), "mlp_norm": w["mlp_norm"].contiguous(),
+                                "w_qkv": qkv, "w_o": wo, "w_gate_up": gu, "w_down": wd})
+            torch.cuda.current_stream().synchronize()
+            del w
+        self.embed = glob["embed"].contiguous()
+        self.final_norm = glob["final_norm"].contiguous()
+        self.lm_head = torch.empty(s.vocab * s.d_model, dtype=dt, device=dev)
+        pack(self.lm_head, glob["lm_head"], s.vocab, s.d_model)
+        torch.cuda.current_stream().synchronize()
+
+        L = s.n_layers
+
+        def arr(key):
+            a = (C.c_void_p * L)(*[self.layers[l][key].data_ptr() for l in range(L)])
+            return a
+
+        self._arrs = {k: arr(k) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")}
+        self.c = wisp_model(L, s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.d_ff, s.vocab,
+                            s.rms_eps, s.rope_base, code, self.embed.data_ptr(), self.final_norm.data_ptr(),
+                            self.lm_head.data_ptr(),
+                            *[C.cast(self._arrs[k], _PVP) for k in ("attn_norm", "w_qkv", "w_o",
+                                                                    "mlp_norm", "w_gate_up", "w_down")])
+
+    @staticmethod
+    def shape_only(shape) -> wisp_model:
+        code = WISP_F32 if shape.dtype == "f32" else WISP_BF16
+        return wisp_model(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                          shape.d_ff, shape.vocab, shape.rms_eps, shape.rope_base, code)
+
+
+# ------------------------------------------------------------------------------------------
+# entry points (C names)
+# ------------------------------------------------------------------------------------------
+def wisp_workspace_size(model: wisp_model, desc: BatchDesc) -> int:
+    return int(lib.wisp_workspace_size(C.byref(model), C.byref(desc.c)))
+
+
+def wisp_accept_workspace_size(desc: BatchDesc) -> int:
+    return int(lib.wisp_accept_workspace_size(C.byref(desc.c)))
+
+
+def wisp_pack_linear(dst, src, rows: int, cols: int, dtype: int, stream=None):
+    _ok(lib.wisp_pack_linear(_ptr(dst), _ptr(src), rows, cols, dtype, _stream(stream)))
+
+
+def wisp_verify(model: wisp_model, kv: KVPool, desc: BatchDesc, tokens, draft_probs, rng_seed: int,
+                accept_len, out_tokens, target_logits, workspace, stream=None):
+    _ok(lib.wisp_verify(C.byref(model), C.byref(kv.c), C.byref(desc.c), _ptr(tokens), _ptr(draft_probs),
+                        rng_seed & ((1 << 64) - 1), _ptr(accept_len), _ptr(out_tokens), _ptr(target_logits),
+                        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def wisp_accept(desc: BatchDesc, vocab: int, logits, tokens, draft_probs, rng_seed: int, accept_len,
+                out_tokens, workspace, stream=None):
+    _ok(lib.wisp_accept(C.byref(desc.c), vocab, _ptr(logits), _ptr(tokens), _ptr(draft_probs),
+                        rng_seed & ((1 << 64) - 1), _ptr(accept_len), _ptr(out_tokens), _ptr(workspace),
+                        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def wisp_attention(model: wisp_model, kv: KVPool, desc: BatchDesc, q, out, workspace, stream=None):
+    _ok(lib.wisp_attention(C.byref(model), C.byref(kv.c), C.byref(desc.c), _ptr(q), _ptr(out),
+                           _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def wisp_uniform(rng_seed: int, req_id: int, tag: int, row: int, n: int, out, stream=None):
+    _ok(lib.wisp_uniform(rng_seed & ((1 << 64) - 1), req_id, tag, row, n, _ptr(out), _stream(stream)))
+
+
+def wisp_check(workspace, stream=None):
+    _ok(lib.wisp_check(_ptr(workspace), _stream(stream)))
+
+
+def workspace(nbytes: int, device="cuda"):
+    """A device byte buffer for the workspace argument (torch allocation)."""
+    import torch
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)

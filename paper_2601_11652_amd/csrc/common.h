@@ -1,0 +1,108 @@
+// Device-side helpers shared by the gfx950 kernels of the verification step.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wisp {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kPage = 16;
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------------------
+// bf16 storage (uint16 bit patterns), round to nearest even; inputs are finite
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack2bf(float a, float b) {
+  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+template <typename T> struct Act;
+template <> struct Act<float> {
+  static __device__ __forceinline__ float load(const float *p, int64_t i) { return p[i]; }
+  static __device__ __forceinline__ void store(float *p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct Act<uint16_t> {
+  static __device__ __forceinline__ float load(const uint16_t *p, int64_t i) { return bf2f(p[i]); }
+  static __device__ __forceinline__ void store(uint16_t *p, int64_t i, float v) { p[i] = f2bf(v); }
+};
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// ---------------------------------------------------------------------------------------
+// KV page layouts (one page = 16 slots x hd of one block and kv head)
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ int k_page_off(int slot, int e) {
+  return ((e >> 5) * 4 + ((e & 31) >> 3)) * 128 + slot * 8 + (e & 7);
+}
+__device__ __forceinline__ int v_page_off(int slot, int e) {
+  return ((e >> 4) * 4 + (slot >> 2)) * 64 + (e & 15) * 4 + (slot & 3);
+}
+
+// Packed GEMM-operand layout: 32 x 16 fragments, fragment (rb, kb) of a matrix with K
+// columns at ((rb * K/16 + kb) * 512); lane l holds row rb*32 + l%32, columns
+// kb*16 + (l/32)*8 + 0..7.
+__device__ __forceinline__ int64_t packed_off(int64_t r, int64_t c, int64_t K) {
+  int64_t rb = r >> 5, kb = c >> 4;
+  int64_t lane = (r & 31) + 32 * ((c & 15) >> 3);
+  return ((rb * (K >> 4) + kb) * 64 + lane) * 8 + (c & 7);
+}
+
+// ---------------------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11) and the uniform draw of the verification stream
+// ---------------------------------------------------------------------------------------
+struct Philox4 {
+  uint32_t v[4];
+};
+
+__device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                                uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  Philox4 o;
+  o.v[0] = c0;
+  o.v[1] = c1;
+  o.v[2] = c2;
+  o.v[3] = c3;
+  return o;
+}
+
+// (2 * (w >> 9) + 1) * 2^-24: exact in fp32, strictly inside (0, 1)
+__device__ __forceinline__ float uniform_from_word(uint32_t w) {
+  return (float)(((w >> 9) << 1) | 1u) * 5.9604644775390625e-8f;
+}
+
+constexpr uint32_t kTagAccept = 1u;
+constexpr uint32_t kTagRace = 2u;
+
+// ---------------------------------------------------------------------------------------
+// error word bits (kept in the first bytes of the workspace)
+// ---------------------------------------------------------------------------------------
+constexpr int kErrToken = 1;
+constexpr int kErrBlock = 2;
+
+__device__ __forceinline__ void flag_error(int *err, int bit) { atomicOr(err, bit); }
+
+}  // namespace wisp

@@ -1,0 +1,77 @@
+// Host-side launchers of the gfx950 kernels (one translation unit per kernel family).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wisp {
+
+// ----- GEMMs: C[z][M][ldc] (fp32) = A[M][K] . W[N][K]^T over the z-th K range ----------
+struct GemmCfg {
+  int bm, bn;       // tile rows / cols
+  int splits;       // K splits (partial sums in fp32, summed in fixed order later)
+  int kf_per_split; // 16-wide K fragments per split
+};
+GemmCfg gemm_bf16_plan(int M, int N, int K);
+void gemm_bf16(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K,
+               int ldc, const GemmCfg &cfg, hipStream_t s);
+void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int ldc, hipStream_t s);
+void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hipStream_t s);
+
+// ----- per-row layers --------------------------------------------------------------------
+struct StepDesc {         // device arrays carved from the workspace
+  const int32_t *off;     // [B+1] first row of request i
+  const int32_t *doff;    // [B+1] first draft row of request i
+  const int32_t *gamma;   // [B]
+  const int32_t *ctx;     // [B]
+  const uint32_t *req_id; // [B]
+  const int32_t *row_req; // [M]
+  const int32_t *row_pos; // [M]
+  const int32_t *page_table;
+  int pt_stride;
+  int n_blocks;
+  int *err;
+};
+
+void rope_table(const StepDesc &d, float *cs, int M, int hd, float base, hipStream_t s);
+
+template <typename T>
+void embed_norm(const StepDesc &d, const T *embed, const T *gain, const int32_t *tokens, float *h,
+                T *xn, bool packed, int M, int dm, int V, float eps, hipStream_t s);
+
+template <typename T>
+void resid_norm(const float *part, int splits, float *h, const T *gain, T *xn, bool packed, int M,
+                int dm, float eps, hipStream_t s);
+
+template <typename T>
+void qkv_rope_append(const StepDesc &d, const float *part, int splits, const float *cs, T *q,
+                     T *k_pool, T *v_pool, int M, int nq, int nkv, int hd, hipStream_t s);
+
+template <typename T>
+void swiglu(const float *part, int splits, T *out, bool packed, int M, int F, hipStream_t s);
+
+// ----- attention ---------------------------------------------------------------------------
+struct AttnItem {   // one wave's work: request, kv head, row group, token range
+  int32_t req, kvh_rbg, t0, t1;
+};
+struct AttnGroup {  // the chunks of one (request, kv head, row group), combined in order
+  int32_t req, kvh, rbg, first_item, n_items, pad0, pad1, pad2;
+};
+constexpr int kAttnRowsPerItem = 64;   // query rows one wave carries (4 blocks of 16)
+
+void attention_bf16(const StepDesc &d, const AttnItem *items, int n_items, const AttnGroup *groups,
+                    int n_groups, const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
+                    float *part_o, float *part_ml, uint16_t *out, bool out_packed, int out_K, int nq,
+                    int nkv, int hd, hipStream_t s);
+void attention_f32(const StepDesc &d, int B, const float *q, const float *k_pool,
+                   const float *v_pool, float *out, int nq, int nkv, int hd, int max_tokens,
+                   hipStream_t s);
+
+// ----- acceptance ----------------------------------------------------------------------------
+void sampler(const StepDesc &d, int B, int M, int V, const float *logits, const int32_t *tokens,
+             const float *q, float T, uint64_t seed, float *row_m, float *row_s, int32_t *row_amax,
+             int32_t *accept_len, int32_t *out_tokens, hipStream_t s);
+void uniform_draws(uint64_t seed, uint32_t req, uint32_t tag, uint32_t row, uint32_t n, float *out,
+                   hipStream_t s);
+void clear_ints(int *p, int n, hipStream_t s);
+
+}  // namespace wisp

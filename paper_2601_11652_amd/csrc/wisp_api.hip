@@ -1,0 +1,519 @@
+// C ABI of the verification step (declared in include/wisp.h): validation, planning of
+// the launch (row layout, GEMM K-splits, split-KV attention work list), workspace carving
+// and the stream-ordered kernel sequence of one step.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/wisp.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace wisp;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+wisp_status fail(wisp_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+wisp_status fail(wisp_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ------------------------------------------------------------------------------------------
+// launch plan
+// ------------------------------------------------------------------------------------------
+struct Plan {
+  int B = 0, M = 0, Mp = 0, S = 0;   // requests, rows, rows padded to 32, total drafts
+  int d = 0, nq = 0, nkv = 0, hd = 0, F = 0, V = 0, qdim = 0, kvdim = 0, qkvN = 0, G = 0;
+  bool bf16 = false;
+  int max_tokens = 0;
+  GemmCfg g_qkv{}, g_o{}, g_gu{}, g_down{}, g_lm{};
+  std::vector<AttnItem> items;
+  std::vector<AttnGroup> groups;
+  std::vector<int32_t> host;         // descriptor block uploaded to the device
+  // int32 offsets inside the descriptor block
+  size_t i_off = 0, i_doff = 0, i_gamma = 0, i_ctx = 0, i_req = 0, i_row_req = 0, i_row_pos = 0,
+         i_items = 0, i_groups = 0;
+  // byte offsets inside the workspace
+  size_t w_err = 0, w_desc = 0, w_rope = 0, w_h = 0, w_xn = 0, w_ao = 0, w_af = 0, w_q = 0,
+         w_part = 0, w_attn_o = 0, w_attn_ml = 0, w_m = 0, w_s = 0, w_amax = 0, total = 0;
+};
+
+constexpr int kAttnTargetItems = 1024;
+
+wisp_status check_model(const wisp_model *m, bool need_weights) {
+  if (!m) return fail(WISP_E_INVALID, "model is NULL");
+  if (m->n_layers <= 0 || m->d_model <= 0 || m->n_q_heads <= 0 || m->n_kv_heads <= 0 ||
+      m->head_dim <= 0 || m->d_ff <= 0 || m->vocab <= 0)
+    return fail(WISP_E_INVALID, "model dimensions must be positive");
+  if (m->dtype != WISP_F32 && m->dtype != WISP_BF16) return fail(WISP_E_UNSUPPORTED, "dtype %d", m->dtype);
+  if (m->n_q_heads % m->n_kv_heads) return fail(WISP_E_UNSUPPORTED, "n_q_heads %% n_kv_heads != 0");
+  if (m->head_dim % 32) return fail(WISP_E_UNSUPPORTED, "head_dim must be a multiple of 32");
+  if (m->d_model % 32 || m->d_ff % 32) return fail(WISP_E_UNSUPPORTED, "d_model, d_ff must be multiples of 32");
+  if (m->d_model > 16384) return fail(WISP_E_UNSUPPORTED, "d_model > 16384");
+  if (m->dtype == WISP_BF16) {
+    if (m->head_dim != 64 && m->head_dim != 128) return fail(WISP_E_UNSUPPORTED, "bf16 head_dim must be 64 or 128");
+    if (m->vocab % 32) return fail(WISP_E_UNSUPPORTED, "bf16 vocab must be a multiple of 32");
+    if (m->n_q_heads / m->n_kv_heads > 64) return fail(WISP_E_UNSUPPORTED, "GQA group > 64");
+  }
+  if (!(m->rms_eps >= 0.f) || !(m->rope_base > 0.f)) return fail(WISP_E_INVALID, "rms_eps / rope_base");
+  if (need_weights) {
+    if (!m->embed || !m->final_norm || !m->lm_head || !m->attn_norm || !m->w_qkv || !m->w_o ||
+        !m->mlp_norm || !m->w_gate_up || !m->w_down)
+      return fail(WISP_E_INVALID, "NULL weight pointer");
+    for (int l = 0; l < m->n_layers; ++l)
+      if (!m->attn_norm[l] || !m->w_qkv[l] || !m->w_o[l] || !m->mlp_norm[l] || !m->w_gate_up[l] ||
+          !m->w_down[l])
+        return fail(WISP_E_INVALID, "NULL weight pointer in layer %d", l);
+  }
+  return WISP_OK;
+}
+
+wisp_status check_desc(const wisp_batch_desc *d, bool need_pages) {
+  if (!d) return fail(WISP_E_INVALID, "batch descriptor is NULL");
+  if (d->B < 0) return fail(WISP_E_INVALID, "B < 0");
+  if (d->B == 0) return WISP_OK;
+  if (!d->ctx_len || !d->gamma) return fail(WISP_E_INVALID, "ctx_len / gamma is NULL");
+  if (!(d->temperature >= 0.f) || std::isinf(d->temperature)) return fail(WISP_E_INVALID, "temperature must be finite and >= 0");
+  for (int i = 0; i < d->B; ++i) {
+    if (d->gamma[i] < 0 || d->gamma[i] > WISP_GAMMA_MAX)
+      return fail(WISP_E_INVALID, "gamma[%d] = %d outside 0..%d", i, d->gamma[i], WISP_GAMMA_MAX);
+    if (d->ctx_len[i] < 0) return fail(WISP_E_INVALID, "ctx_len[%d] < 0", i);
+    if (need_pages && (int64_t)d->pt_stride * WISP_PAGE < (int64_t)d->ctx_len[i] + d->gamma[i] + 1)
+      return fail(WISP_E_CAPACITY, "request %d needs %d tokens but the page table holds %d", i,
+                  d->ctx_len[i] + d->gamma[i] + 1, d->pt_stride * WISP_PAGE);
+  }
+  if (need_pages && !d->kv_page_table) return fail(WISP_E_INVALID, "kv_page_table is NULL");
+  return WISP_OK;
+}
+
+void carve(Plan &p, size_t &w, size_t &field, size_t bytes) {
+  field = w;
+  w = align256(w + bytes);
+}
+
+// forward=true: the full step; false: acceptance only (rows/drafts of the batch)
+void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward) {
+  p.B = d->B;
+  std::vector<int> off(p.B + 1, 0), doff(p.B + 1, 0);
+  for (int i = 0; i < p.B; ++i) {
+    off[i + 1] = off[i] + d->gamma[i] + 1;
+    doff[i + 1] = doff[i] + d->gamma[i];
+  }
+  p.M = off[p.B];
+  p.S = doff[p.B];
+  p.Mp = (p.M + 31) / 32 * 32;
+  if (forward) {
+    p.d = m->d_model;
+    p.nq = m->n_q_heads;
+    p.nkv = m->n_kv_heads;
+    p.hd = m->head_dim;
+    p.F = m->d_ff;
+    p.V = m->vocab;
+    p.G = p.nq / p.nkv;
+    p.qdim = p.nq * p.hd;
+    p.kvdim = p.nkv * p.hd;
+    p.qkvN = p.qdim + 2 * p.kvdim;
+    p.bf16 = m->dtype == WISP_BF16;
+    for (int i = 0; i < p.B; ++i) p.max_tokens = std::max(p.max_tokens, d->ctx_len[i] + d->gamma[i] + 1);
+    if (p.bf16) {
+      p.g_qkv = gemm_bf16_plan(p.M, p.qkvN, p.d);
+      p.g_o = gemm_bf16_plan(p.M, p.d, p.qdim);
+      p.g_gu = gemm_bf16_plan(p.M, 2 * p.F, p.d);
+      p.g_down = gemm_bf16_plan(p.M, p.d, p.F);
+      p.g_lm = gemm_bf16_plan(p.M, p.V, p.d);
+      p.g_lm.splits = 1;
+      p.g_lm.kf_per_split = p.d / 16;
+      // split-KV work list: items of <= 64 query rows and a chunk of page pairs
+      int64_t units = 0;
+      for (int i = 0; i < p.B; ++i) {
+        const int rows = (d->gamma[i] + 1) * p.G;
+        const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
+        units += (int64_t)nrbg * p.nkv * ((d->ctx_len[i] + d->gamma[i] + 1 + 31) / 32);
+      }
+      int chunk_pairs = (int)std::max<int64_t>(2, (units + kAttnTargetItems - 1) / kAttnTargetItems);
+      const int chunk = 32 * chunk_pairs;
+      for (int i = 0; i < p.B; ++i) {
+        const int T = d->ctx_len[i] + d->gamma[i] + 1;
+        const int rows = (d->gamma[i] + 1) * p.G;
+        const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
+        for (int h = 0; h < p.nkv; ++h)
+          for (int g = 0; g < nrbg; ++g) {
+            AttnGroup gr{};
+            gr.req = i;
+            gr.kvh = h;
+            gr.rbg = g;
+            gr.first_item = (int32_t)p.items.size();
+            for (int t0 = 0; t0 < T; t0 += chunk) {
+              AttnItem it{};
+              it.req = i;
+              it.kvh_rbg = h | (g << 16);
+              it.t0 = t0;
+              it.t1 = std::min(T, t0 + chunk);
+              p.items.push_back(it);
+            }
+            gr.n_items = (int32_t)p.items.size() - gr.first_item;
+            p.groups.push_back(gr);
+          }
+      }
+    }
+  }
+  // descriptor block
+  size_t n = 0;
+  auto take = [&](size_t &f, size_t cnt) {
+    f = n;
+    n += (cnt + 63) / 64 * 64;
+  };
+  take(p.i_off, p.B + 1);
+  take(p.i_doff, p.B + 1);
+  take(p.i_gamma, p.B);
+  take(p.i_ctx, p.B);
+  take(p.i_req, p.B);
+  take(p.i_row_req, p.M);
+  take(p.i_row_pos, p.M);
+  take(p.i_items, p.items.size() * 4);
+  take(p.i_groups, p.groups.size() * 8);
+  p.host.assign(n, 0);
+  for (int i = 0; i <= p.B; ++i) {
+    p.host[p.i_off + i] = off[i];
+    p.host[p.i_doff + i] = doff[i];
+  }
+  for (int i = 0; i < p.B; ++i) {
+    p.host[p.i_gamma + i] = d->gamma[i];
+    p.host[p.i_ctx + i] = d->ctx_len[i];
+    p.host[p.i_req + i] = d->req_id ? (int32_t)d->req_id[i] : i;
+    for (int j = 0; j <= d->gamma[i]; ++j) {
+      p.host[p.i_row_req + off[i] + j] = i;
+      p.host[p.i_row_pos + off[i] + j] = d->ctx_len[i] + j;
+    }
+  }
+  if (!p.items.empty()) std::memcpy(&p.host[p.i_items], p.items.data(), p.items.size() * sizeof(AttnItem));
+  if (!p.groups.empty()) std::memcpy(&p.host[p.i_groups], p.groups.data(), p.groups.size() * sizeof(AttnGroup));
+
+  // workspace
+  size_t w = 0;
+  carve(p, w, p.w_err, 256);
+  carve(p, w, p.w_desc, p.host.size() * sizeof(int32_t));
+  carve(p, w, p.w_m, (size_t)p.M * 4);
+  carve(p, w, p.w_s, (size_t)p.M * 4);
+  carve(p, w, p.w_amax, (size_t)p.M * 4);
+  if (forward) {
+    const size_t es = p.bf16 ? 2 : 4;
+    carve(p, w, p.w_rope, (size_t)p.M * p.hd * 4);
+    carve(p, w, p.w_h, (size_t)p.M * p.d * 4);
+    carve(p, w, p.w_xn, (size_t)p.Mp * p.d * es);
+    carve(p, w, p.w_ao, (size_t)p.Mp * p.qdim * es);
+    carve(p, w, p.w_af, (size_t)p.Mp * p.F * es);
+    carve(p, w, p.w_q, (size_t)p.M * p.qdim * es);
+    size_t part = 0;
+    if (p.bf16) {
+      part = std::max({(size_t)p.g_qkv.splits * p.qkvN, (size_t)p.g_o.splits * p.d,
+                       (size_t)p.g_gu.splits * 2 * p.F, (size_t)p.g_down.splits * p.d});
+    } else {
+      part = std::max({(size_t)p.qkvN, (size_t)p.d, (size_t)2 * p.F});
+    }
+    carve(p, w, p.w_part, part * p.M * 4);
+    carve(p, w, p.w_attn_o, p.items.size() * (size_t)p.hd * 64 * 4);
+    carve(p, w, p.w_attn_ml, p.items.size() * 64 * 2 * 4);
+  }
+  p.total = w;
+}
+
+// pinned staging for the descriptor upload, reused once the previous copy has finished
+struct Staging {
+  void *buf = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+thread_local Staging g_stage;
+
+wisp_status upload(const Plan &p, char *ws, hipStream_t s) {
+  const size_t bytes = p.host.size() * sizeof(int32_t);
+  if (bytes == 0) return WISP_OK;
+  if (g_stage.pending) {
+    if (hipEventSynchronize(g_stage.ev) != hipSuccess) return fail(WISP_E_HIP, "staging event sync failed");
+    g_stage.pending = false;
+  }
+  if (g_stage.cap < bytes) {
+    if (g_stage.buf) (void)hipHostFree(g_stage.buf);
+    g_stage.buf = nullptr;
+    g_stage.cap = 0;
+    size_t cap = std::max<size_t>(bytes, 1 << 16);
+    if (hipHostMalloc(&g_stage.buf, cap, hipHostMallocDefault) != hipSuccess)
+      return fail(WISP_E_HIP, "pinned staging allocation failed");
+    g_stage.cap = cap;
+  }
+  if (!g_stage.ev && hipEventCreateWithFlags(&g_stage.ev, hipEventDisableTiming) != hipSuccess)
+    return fail(WISP_E_HIP, "event creation failed");
+  std::memcpy(g_stage.buf, p.host.data(), bytes);
+  if (hipMemcpyAsync(ws + p.w_desc, g_stage.buf, bytes, hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(WISP_E_HIP, "descriptor upload failed");
+  if (hipEventRecord(g_stage.ev, s) != hipSuccess) return fail(WISP_E_HIP, "event record failed");
+  g_stage.pending = true;
+  return WISP_OK;
+}
+
+StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_blocks) {
+  const int32_t *base = reinterpret_cast<const int32_t *>(ws + p.w_desc);
+  StepDesc sd;
+  sd.off = base + p.i_off;
+  sd.doff = base + p.i_doff;
+  sd.gamma = base + p.i_gamma;
+  sd.ctx = base + p.i_ctx;
+  sd.req_id = reinterpret_cast<const uint32_t *>(base + p.i_req);
+  sd.row_req = base + p.i_row_req;
+  sd.row_pos = base + p.i_row_pos;
+  sd.page_table = d->kv_page_table;
+  sd.pt_stride = d->pt_stride;
+  sd.n_blocks = n_blocks;
+  sd.err = reinterpret_cast<int *>(ws + p.w_err);
+  return sd;
+}
+
+wisp_status hip_check(const char *what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(WISP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  return WISP_OK;
+}
+
+template <typename T>
+wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, const StepDesc &sd,
+                        char *ws, const int32_t *tokens, float *logits, hipStream_t s) {
+  const bool packed = p.bf16;
+  float *cs = reinterpret_cast<float *>(ws + p.w_rope);
+  float *h = reinterpret_cast<float *>(ws + p.w_h);
+  T *xn = reinterpret_cast<T *>(ws + p.w_xn);
+  T *ao = reinterpret_cast<T *>(ws + p.w_ao);
+  T *af = reinterpret_cast<T *>(ws + p.w_af);
+  T *qb = reinterpret_cast<T *>(ws + p.w_q);
+  float *part = reinterpret_cast<float *>(ws + p.w_part);
+  const int64_t layer_elems = (int64_t)kv->n_blocks * p.nkv * WISP_PAGE * p.hd;
+  const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
+  const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
+
+  rope_table(sd, cs, p.M, p.hd, m->rope_base, s);
+  embed_norm<T>(sd, (const T *)m->embed, (const T *)m->attn_norm[0], tokens, h, xn, packed, p.M, p.d,
+                p.V, m->rms_eps, s);
+  for (int l = 0; l < m->n_layers; ++l) {
+    T *kl = (T *)kv->k_pool + l * layer_elems;
+    T *vl = (T *)kv->v_pool + l * layer_elems;
+    int sq = 1, so = 1, sg = 1, sdn = 1;
+    if (p.bf16) {
+      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->w_qkv[l], part, p.M, p.qkvN, p.d, p.qkvN, p.g_qkv, s);
+      sq = p.g_qkv.splits;
+    } else {
+      gemm_f32((const float *)xn, (const float *)m->w_qkv[l], part, p.M, p.qkvN, p.d, p.qkvN, s);
+    }
+    qkv_rope_append<T>(sd, part, sq, cs, qb, kl, vl, p.M, p.nq, p.nkv, p.hd, s);
+    if (p.bf16) {
+      attention_bf16(sd, items, (int)p.items.size(), groups, (int)p.groups.size(), (const uint16_t *)qb,
+                     (const uint16_t *)kl, (const uint16_t *)vl, reinterpret_cast<float *>(ws + p.w_attn_o),
+                     reinterpret_cast<float *>(ws + p.w_attn_ml), (uint16_t *)ao, true, p.qdim, p.nq,
+                     p.nkv, p.hd, s);
+      gemm_bf16((const uint16_t *)ao, (const uint16_t *)m->w_o[l], part, p.M, p.d, p.qdim, p.d, p.g_o, s);
+      so = p.g_o.splits;
+    } else {
+      attention_f32(sd, p.B, (const float *)qb, (const float *)kl, (const float *)vl, (float *)ao, p.nq,
+                    p.nkv, p.hd, p.max_tokens, s);
+      gemm_f32((const float *)ao, (const float *)m->w_o[l], part, p.M, p.d, p.qdim, p.d, s);
+    }
+    resid_norm<T>(part, so, h, (const T *)m->mlp_norm[l], xn, packed, p.M, p.d, m->rms_eps, s);
+    if (p.bf16) {
+      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->w_gate_up[l], part, p.M, 2 * p.F, p.d, 2 * p.F, p.g_gu, s);
+      sg = p.g_gu.splits;
+    } else {
+      gemm_f32((const float *)xn, (const float *)m->w_gate_up[l], part, p.M, 2 * p.F, p.d, 2 * p.F, s);
+    }
+    swiglu<T>(part, sg, af, packed, p.M, p.F, s);
+    if (p.bf16) {
+      gemm_bf16((const uint16_t *)af, (const uint16_t *)m->w_down[l], part, p.M, p.d, p.F, p.d, p.g_down, s);
+      sdn = p.g_down.splits;
+    } else {
+      gemm_f32((const float *)af, (const float *)m->w_down[l], part, p.M, p.d, p.F, p.d, s);
+    }
+    const T *gain = (l + 1 < m->n_layers) ? (const T *)m->attn_norm[l + 1] : (const T *)m->final_norm;
+    resid_norm<T>(part, sdn, h, gain, xn, packed, p.M, p.d, m->rms_eps, s);
+  }
+  if (p.bf16)
+    gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.M, p.V, p.d, p.V, p.g_lm, s);
+  else
+    gemm_f32((const float *)xn, (const float *)m->lm_head, logits, p.M, p.V, p.d, p.V, s);
+  return hip_check("forward launch");
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------------
+// exported entry points
+// ------------------------------------------------------------------------------------------
+extern "C" {
+
+const char *wisp_last_error(void) { return g_last_error.c_str(); }
+
+size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc) {
+  if (check_model(model, false) != WISP_OK || check_desc(desc, false) != WISP_OK) return 0;
+  Plan p;
+  make_plan(p, model, desc, true);
+  return p.total;
+}
+
+size_t wisp_accept_workspace_size(const wisp_batch_desc *desc) {
+  if (check_desc(desc, false) != WISP_OK) return 0;
+  Plan p;
+  make_plan(p, nullptr, desc, false);
+  return p.total;
+}
+
+wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t cols, int32_t dtype,
+                             void *stream) {
+  if (!dst || !src) return fail(WISP_E_INVALID, "NULL pointer");
+  if (rows <= 0 || cols <= 0) return fail(WISP_E_INVALID, "rows, cols must be positive");
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == WISP_BF16) {
+    if (rows % 32 || cols % 16) return fail(WISP_E_UNSUPPORTED, "bf16 packing needs rows %% 32 == 0 and cols %% 16 == 0");
+    pack_linear_bf16((uint16_t *)dst, (const uint16_t *)src, rows, cols, s);
+  } else if (dtype == WISP_F32) {
+    if (hipMemcpyAsync(dst, src, (size_t)rows * cols * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+      return fail(WISP_E_HIP, "copy failed");
+  } else {
+    return fail(WISP_E_UNSUPPORTED, "dtype %d", dtype);
+  }
+  return hip_check("pack");
+}
+
+wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                        const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
+                        int32_t *accept_len, int32_t *out_tokens, float *target_logits,
+                        void *workspace, size_t workspace_bytes, void *stream) {
+  wisp_status st;
+  if ((st = check_model(model, true)) != WISP_OK) return st;
+  if ((st = check_desc(desc, true)) != WISP_OK) return st;
+  if (desc->B == 0) return WISP_OK;
+  if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
+  if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
+  if (kv->n_blocks <= 0) return fail(WISP_E_INVALID, "n_blocks must be positive");
+  if (!tokens || !accept_len || !out_tokens || !target_logits || !workspace)
+    return fail(WISP_E_INVALID, "NULL tokens / outputs / workspace");
+  Plan p;
+  make_plan(p, model, desc, true);
+  if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
+  if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
+  if (workspace_bytes < p.total)
+    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
+  hipStream_t s = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  if ((st = upload(p, ws, s)) != WISP_OK) return st;
+  StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
+  clear_ints(sd.err, 1, s);
+  if (p.bf16)
+    st = run_forward<uint16_t>(p, model, kv, sd, ws, tokens, target_logits, s);
+  else
+    st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
+  if (st != WISP_OK) return st;
+  sampler(sd, p.B, p.M, p.V, target_logits, tokens, draft_probs, desc->temperature, rng_seed,
+          reinterpret_cast<float *>(ws + p.w_m), reinterpret_cast<float *>(ws + p.w_s),
+          reinterpret_cast<int32_t *>(ws + p.w_amax), accept_len, out_tokens, s);
+  return hip_check("sampler launch");
+}
+
+wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float *logits,
+                        const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
+                        int32_t *accept_len, int32_t *out_tokens, void *workspace,
+                        size_t workspace_bytes, void *stream) {
+  wisp_status st;
+  if ((st = check_desc(desc, false)) != WISP_OK) return st;
+  if (desc->B == 0) return WISP_OK;
+  if (vocab <= 0) return fail(WISP_E_INVALID, "vocab must be positive");
+  if (!logits || !tokens || !accept_len || !out_tokens || !workspace)
+    return fail(WISP_E_INVALID, "NULL logits / tokens / outputs / workspace");
+  Plan p;
+  make_plan(p, nullptr, desc, false);
+  if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
+  if (workspace_bytes < p.total)
+    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
+  hipStream_t s = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  if ((st = upload(p, ws, s)) != WISP_OK) return st;
+  StepDesc sd = step_desc(p, ws, desc, 0);
+  clear_ints(sd.err, 1, s);
+  sampler(sd, p.B, p.M, vocab, logits, tokens, draft_probs, desc->temperature, rng_seed,
+          reinterpret_cast<float *>(ws + p.w_m), reinterpret_cast<float *>(ws + p.w_s),
+          reinterpret_cast<int32_t *>(ws + p.w_amax), accept_len, out_tokens, s);
+  return hip_check("sampler launch");
+}
+
+wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                           const void *q, void *out, void *workspace, size_t workspace_bytes,
+                           void *stream) {
+  wisp_status st;
+  if ((st = check_model(model, false)) != WISP_OK) return st;
+  if ((st = check_desc(desc, true)) != WISP_OK) return st;
+  if (desc->B == 0) return WISP_OK;
+  if (!kv || !kv->k_pool || !kv->v_pool || kv->n_blocks <= 0) return fail(WISP_E_INVALID, "KV pools");
+  if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
+  if (!q || !out || !workspace) return fail(WISP_E_INVALID, "NULL q / out / workspace");
+  Plan p;
+  make_plan(p, model, desc, true);
+  if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
+  if (workspace_bytes < p.total)
+    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
+  hipStream_t s = (hipStream_t)stream;
+  char *ws = (char *)workspace;
+  if ((st = upload(p, ws, s)) != WISP_OK) return st;
+  StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
+  clear_ints(sd.err, 1, s);
+  if (p.bf16) {
+    const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
+    const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
+    attention_bf16(sd, items, (int)p.items.size(), groups, (int)p.groups.size(), (const uint16_t *)q,
+                   (const uint16_t *)kv->k_pool, (const uint16_t *)kv->v_pool,
+                   reinterpret_cast<float *>(ws + p.w_attn_o), reinterpret_cast<float *>(ws + p.w_attn_ml),
+                   (uint16_t *)out, false, p.qdim, p.nq, p.nkv, p.hd, s);
+  } else {
+    attention_f32(sd, p.B, (const float *)q, (const float *)kv->k_pool, (const float *)kv->v_pool,
+                  (float *)out, p.nq, p.nkv, p.hd, p.max_tokens, s);
+  }
+  return hip_check("attention launch");
+}
+
+wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint32_t row, uint32_t n,
+                         float *out, void *stream) {
+  if (!out && n) return fail(WISP_E_INVALID, "out is NULL");
+  uniform_draws(rng_seed, req_id, tag, row, n, out, (hipStream_t)stream);
+  return hip_check("uniform launch");
+}
+
+wisp_status wisp_check(void *workspace, void *stream) {
+  if (!workspace) return fail(WISP_E_INVALID, "workspace is NULL");
+  hipStream_t s = (hipStream_t)stream;
+  if (hipStreamSynchronize(s) != hipSuccess) return fail(WISP_E_HIP, "stream synchronize failed");
+  int err = 0;
+  if (hipMemcpy(&err, workspace, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+    return fail(WISP_E_HIP, "error word read failed");
+  if (err) {
+    int zero = 0;
+    (void)hipMemcpy(workspace, &zero, sizeof(int), hipMemcpyHostToDevice);
+    return fail(WISP_E_DEVICE_INPUT, "device-side input check failed:%s%s",
+                (err & kErrToken) ? " token id out of range" : "",
+                (err & kErrBlock) ? " block id out of range" : "");
+  }
+  return WISP_OK;
+}
+
+}  // extern "C"

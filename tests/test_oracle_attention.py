@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 
 import oracle
+import wisp_inputs as wi
 
 PAGE = 16
 
@@ -26,8 +27,8 @@ def _case(B, n_q, n_kv, hd, seed, bf16):
     for i in range(B):
         pt[i, :need[i]] = perm[o:o + need[i]]
         o += need[i]
-    kd = rng.standard_normal((n_blocks, n_kv, PAGE, hd))
-    vd = rng.standard_normal((n_blocks, n_kv, hd, PAGE))
+    kd = rng.standard_normal((n_blocks, n_kv, PAGE, hd))     # [block][kv][slot][dim]
+    vd = rng.standard_normal((n_blocks, n_kv, PAGE, hd))
     if bf16:
         kd, vd = oracle.round_bf16(kd).reshape(kd.shape), oracle.round_bf16(vd).reshape(vd.shape)
         kp = (kd.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
@@ -35,6 +36,7 @@ def _case(B, n_q, n_kv, hd, seed, bf16):
     else:
         kd, vd = kd.astype(np.float32).astype(np.float64), vd.astype(np.float32).astype(np.float64)
         kp, vp = kd.astype(np.float32), vd.astype(np.float32)
+    kp, vp = wi.pages_from_slots(kp, "k"), wi.pages_from_slots(vp, "v")
     M = int(n_new.sum())
     q = rng.standard_normal((M, n_q, hd))
     return ctx, n_new, pt, kd, vd, kp, vp, q
@@ -52,7 +54,7 @@ def _brute(ctx, n_new, pt, kd, vd, q, n_kv):
         for j in range(n_new[i]):
             for h in range(n_q):
                 K = kd[blk, h // G, slot, :]              # [T][hd]
-                Vv = vd[blk, h // G, :, slot]             # [T][hd]
+                Vv = vd[blk, h // G, slot, :]             # [T][hd]
                 s = K @ q[r, h] / np.sqrt(hd)
                 s[ctx[i] + j + 1:] = -np.inf              # causal: keys <= own position
                 w = np.exp(s - s.max())
@@ -79,4 +81,4 @@ def test_empty_context_row_sees_only_itself():
     for i in range(3):
         blk = pt[i, 0]
         for h in range(4):
-            np.testing.assert_allclose(got[i, h], vd[blk, h, :, 0], rtol=1e-12)
+            np.testing.assert_allclose(got[i, h], vd[blk, h, 0, :], rtol=1e-12)

@@ -127,7 +127,9 @@ def _dense_forward(shape, layers, glob, pools, pt, ctx, n_new, toks):
     hd = shape.head_dim
     kp = torch.from_numpy(pools[0].astype(np.int32) << 16).view(torch.float32) if bf16 else torch.from_numpy(pools[0])
     vp = torch.from_numpy(pools[1].astype(np.int32) << 16).view(torch.float32) if bf16 else torch.from_numpy(pools[1])
-    kp, vp = kp.to(torch.float64), vp.to(torch.float64)
+    # pages -> [layer][block][kv][slot][dim]
+    kp = wi.slots_from_pages(kp.to(torch.float64), "k", hd)
+    vp = wi.slots_from_pages(vp.to(torch.float64), "v", hd)
     out = []
     off = 0
     for i in range(len(ctx)):
@@ -149,7 +151,7 @@ def _dense_forward(shape, layers, glob, pools, pt, ctx, n_new, toks):
             k = _store(_rope_complex(k, pos, shape.rope_base), bf16)
             v = _store(v, bf16)
             kc = kp[l][blk, :, tpos % 16, :]                       # [c][n_kv][hd]
-            vc = vp[l][blk, :, :, tpos % 16]                       # [c][n_kv][hd]
+            vc = vp[l][blk, :, tpos % 16, :]                       # [c][n_kv][hd]
             K = torch.cat([kc, k], 0).repeat_interleave(G, dim=1).transpose(0, 1)   # [n_q][T][hd]
             Vv = torch.cat([vc, v], 0).repeat_interleave(G, dim=1).transpose(0, 1)
             T = c + n

@@ -151,6 +151,44 @@ def kv_values(seed: int, layer: int, req: int, start_pos: int, n_pos: int, n_kv:
 
 
 # --------------------------------------------------------------------------------------
+# KV page placement (the documented page layout; used to place inputs and read pages)
+# --------------------------------------------------------------------------------------
+def k_page_index(hd: int) -> np.ndarray:
+    """[16][hd] -> flat position inside a K page: ((e/32)*4 + (e%32)/8)*128 + s*8 + e%8."""
+    s = np.arange(PAGE)[:, None]
+    e = np.arange(hd)[None, :]
+    return ((e // 32) * 4 + (e % 32) // 8) * 128 + s * 8 + e % 8
+
+
+def v_page_index(hd: int) -> np.ndarray:
+    """[16][hd] -> flat position inside a V page: ((e/16)*4 + s/4)*64 + (e%16)*4 + s%4."""
+    s = np.arange(PAGE)[:, None]
+    e = np.arange(hd)[None, :]
+    return ((e // 16) * 4 + s // 4) * 64 + (e % 16) * 4 + s % 4
+
+
+def pages_from_slots(x, which: str):
+    """x [..., 16, hd] (slot-major) -> [..., 16*hd] pages in the K or V page layout."""
+    hd = x.shape[-1]
+    idx = (k_page_index if which == "k" else v_page_index)(hd).reshape(-1)
+    if isinstance(x, torch.Tensor):
+        out = torch.empty(*x.shape[:-2], PAGE * hd, dtype=x.dtype, device=x.device)
+        out[..., torch.as_tensor(idx, device=x.device)] = x.reshape(*x.shape[:-2], -1)
+        return out
+    out = np.empty(x.shape[:-2] + (PAGE * hd,), dtype=x.dtype)
+    out[..., idx] = x.reshape(x.shape[:-2] + (-1,))
+    return out
+
+
+def slots_from_pages(p, which: str, hd: int):
+    """Inverse of pages_from_slots: [..., 16*hd] -> [..., 16, hd]."""
+    idx = (k_page_index if which == "k" else v_page_index)(hd)
+    if isinstance(p, torch.Tensor):
+        return p[..., torch.as_tensor(idx, device=p.device)]
+    return p[..., idx]
+
+
+# --------------------------------------------------------------------------------------
 # model weights (natural layout: every linear map is [out_features][in_features])
 # --------------------------------------------------------------------------------------
 WEIGHT_STD = 0.02
