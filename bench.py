@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched speculative-verification step (WISP, Sec. 4.5) on one MI355X.
+
+Workload (default): Llama-3-8B-shaped random-init model in bf16 (32 layers, d 4096,
+32 q / 8 kv heads x 128, SwiGLU 14336, vocab 128256), B = 32 requests with cached
+contexts U[512, 2048] in 16-token pages and gamma U{1..8} drafts, draft distributions
+q = softmax(logits / T + N(0, 0.5)) with T ~ U[0.8, 1.2] per request.
+
+One step = one wisp_verify call: forward of all sum(gamma+1) rows over the paged KV plus
+acceptance.  Inputs are resident in HBM before timing; the call is idempotent, so the
+same batch is verified W + K times.  Metric: committed (accepted + extra) tokens per
+second, sum(L_i + 1) / step time, with the step latency alongside.
+
+Prints ONE JSON line.  Also reports the dominant kernel class against its roofline
+(algorithmic bytes per launch over the HIP-event-timed average launch) and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6
+FP32_PEAK_TFLOPS = 157.3
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def fill_kv_device(kv, mix, pt_np):
+    """Synthetic cached context of every request, generated on the device and placed
+    through the page table in the documented page layout."""
+    import torch
+    import wisp_inputs as wi
+    s = mix.shape
+    dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
+    kidx = torch.as_tensor(wi.k_page_index(s.head_dim), device="cuda")
+    vidx = torch.as_tensor(wi.v_page_index(s.head_dim), device="cuda")
+    heads = torch.arange(s.n_kv_heads, device="cuda")[None, :, None]
+    for i in range(mix.B):
+        n = int(mix.ctx_len[i])
+        if n == 0:
+            continue
+        t = torch.arange(n, device="cuda")
+        blk = torch.as_tensor(pt_np[i], device="cuda")[t // 16][:, None, None]
+        slot = t % 16
+        for l in range(s.n_layers):
+            K, V = wi.kv_values(mix.seed, l, i, 0, n, s.n_kv_heads, s.head_dim, "cuda", dt)
+            kv.k[l][blk, heads, kidx[slot][:, None, :]] = K
+            kv.v[l][blk, heads, vidx[slot][:, None, :]] = V
+
+
+def gpu_draft_fixture(W, gm, kv, mix, pt, roots):
+    """Draft tokens and q rows for the timed batch: q_j = softmax(l_{j-1} / T_i + sigma_i eps)
+    from the target's own row j-1 (gamma = 0 verification calls), y_j ~ q_j."""
+    import numpy as np
+    import torch
+    s = mix.shape
+    V = s.vocab
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(mix.seed * 7 + 5)
+    toks = {i: [int(roots[i])] for i in range(mix.B)}
+    qs = {i: [] for i in range(mix.B)}
+    for j in range(1, int(mix.gamma.max()) + 1):
+        act = [i for i in range(mix.B) if mix.gamma[i] >= j]
+        a = torch.as_tensor(act, device="cuda")
+        ptj = pt.index_select(0, a).contiguous()
+        desc = W.BatchDesc(mix.ctx_len[act] + j - 1, np.zeros(len(act), np.int32), ptj, 1.0, mix.req_id[act])
+        ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
+        tk = torch.as_tensor([toks[i][j - 1] for i in act], dtype=torch.int32, device="cuda")
+        logits = torch.empty(len(act), V, dtype=torch.float32, device="cuda")
+        acc = torch.empty(len(act), dtype=torch.int32, device="cuda")
+        out = torch.empty(len(act), dtype=torch.int32, device="cuda")
+        W.wisp_verify(gm.c, kv, desc, tk, None, 12345 + j, acc, out, logits, ws)
+        T = torch.as_tensor(mix.t_draft[act], dtype=torch.float32, device="cuda")[:, None]
+        sg = torch.as_tensor(mix.sigma[act], dtype=torch.float32, device="cuda")[:, None]
+        z = logits / T + sg * torch.randn(logits.shape, generator=gen, device="cuda")
+        q = torch.softmax(z, dim=-1)
+        y = torch.multinomial(q, 1, generator=gen)[:, 0].cpu().numpy()
+        for r, i in enumerate(act):
+            toks[i].append(int(y[r]))
+            qs[i].append(q[r])
+    tokens = torch.as_tensor(np.concatenate([toks[i] for i in range(mix.B)]), dtype=torch.int32, device="cuda")
+    qrows = [r for i in range(mix.B) for r in qs[i]]
+    q = torch.stack(qrows).contiguous() if qrows else torch.zeros(1, V, device="cuda")
+    return tokens, q
+
+
+def traffic_from_counters(kernel_key: str):
+    """HBM bytes per launch from committed counter runs, if they were taken on the current
+    kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_key}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(mix, sample_req: int):
+    """The CPU oracle on one request of the same workload (same weights, context KV, root
+    token and gamma; its drafts come from the oracle's own fixture).  Times the oracle's
+    verification of that request: forward of its gamma+1 rows plus acceptance."""
+    import numpy as np
+    import oracle
+    import wisp_inputs as wi
+    from oracle import fixtures as fx
+    s = mix.shape
+    t0 = time.time()
+    model = fx.host_model(s, mix.seed)
+    log(f"cpu baseline: host weights generated in {time.time() - t0:.1f} s")
+    i = sample_req
+    sub = wi.custom_mix(s, [mix.ctx_len[i]], [mix.gamma[i]], seed=mix.seed, name=mix.config)
+    sub.t_draft[:] = mix.t_draft[i]
+    sub.sigma[:] = mix.sigma[i]
+    n_pages = (int(mix.ctx_len[i]) + int(mix.gamma[i]) + 1 + 15) // 16
+    pt = np.arange(n_pages, dtype=np.int32)[None, :]
+    pools = fx.empty_pools(s, n_pages)
+    fx.place_synthetic_kv(sub, pools, pt, req_keys=[i])
+    roots = wi.root_tokens(mix)[i:i + 1]
+    work = (pools[0].copy(), pools[1].copy())
+    toks, qs, _ = fx.draft_fixture(model, sub, work, pt, roots)
+    t1 = time.time()
+    logits = oracle.forward(model, pools[0], pools[1], pt, sub.ctx_len, sub.rows, toks[0])
+    res = oracle.accept(logits, toks[0], qs[0], sub.gamma, 1.0, wi.verify_seed(mix), req_id=[i])
+    dt = time.time() - t1
+    committed = int(res.accept_len[0]) + 1
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": committed / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"request {i} of the {mix.config} batch (ctx {int(mix.ctx_len[i])}, gamma "
+                       f"{int(mix.gamma[i])}): forward of its {int(mix.gamma[i]) + 1} rows through all "
+                       f"{s.n_layers} layers plus acceptance, {committed} committed tokens in {dt:.2f} s")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="8b_b32")
+    ap.add_argument("--B", type=int, default=None, help="override the batch size (sweeps)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for HBM counter scaling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one MI355X only; --gpus {args.gpus} is not supported (requests are "
+              "independent, so N GPUs run N replicas; see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2601_11652_amd as W
+    import wisp_inputs as wi
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    mix = wi.make_mix(args.config, B=args.B)
+    s = mix.shape
+    t0 = time.time()
+    gm = W.GpuModel(s, lambda l: wi.layer_weights(s, l, mix.seed, "cuda"), wi.global_weights(s, mix.seed, "cuda"))
+    log(f"weights generated and packed in {time.time() - t0:.1f} s")
+    pt_np, n_blocks = wi.page_table(mix)
+    dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
+    kv = W.KVPool.zeros(s.n_layers, n_blocks, s.n_kv_heads, s.head_dim, dt)
+    t0 = time.time()
+    fill_kv_device(kv, mix, pt_np)
+    torch.cuda.synchronize()
+    log(f"KV pool {kv.k.numel() * 2 * kv.k.element_size() / 2**30:.2f} GiB filled in {time.time() - t0:.1f} s")
+    pt = torch.as_tensor(pt_np, device="cuda")
+    roots = wi.root_tokens(mix)
+    tokens, q = gpu_draft_fixture(W, gm, kv, mix, pt, roots)
+    log("draft fixture ready")
+
+    desc = W.BatchDesc(mix.ctx_len, mix.gamma, pt, 1.0, mix.req_id)
+    ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
+    M = mix.M
+    acc = torch.empty(mix.B, dtype=torch.int32, device="cuda")
+    out = torch.empty(M, dtype=torch.int32, device="cuda")
+    logits = torch.empty(M, s.vocab, dtype=torch.float32, device="cuda")
+    seed = wi.verify_seed(mix)
+
+    def step():
+        W.wisp_verify(gm.c, kv, desc, tokens, q, seed, acc, out, logits, ws)
+
+    for _ in range(args.warmup):
+        step()
+    W.wisp_check(ws)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = e0.elapsed_time(e1) / args.steps
+    log(f"{args.steps} steps: {ms_step:.3f} ms/step (events), {wall / args.steps * 1e3:.3f} ms/step (wall)")
+    L = acc.cpu().numpy()
+    committed = int((L + 1).sum())
+    value = committed / (ms_step / 1e3)
+
+    # per-kernel-class durations: HIP events around each launch on the library's stream
+    prof_steps = max(3, min(10, args.steps))
+    W.lib.wisp_profile_enable(1)
+    W.lib.wisp_profile_reset()
+    for _ in range(prof_steps):
+        step()
+    torch.cuda.synchronize()
+    classes = {}
+    import ctypes as C
+    for kind, name in ((0, "gemm"), (1, "attention"), (2, "rows"), (3, "sampler")):
+        ms, n, by, fl = C.c_double(), C.c_int64(), C.c_double(), C.c_double()
+        W.lib.wisp_profile_read(kind, C.byref(ms), C.byref(n), C.byref(by), C.byref(fl))
+        if n.value:
+            classes[name] = {"ms_per_step": ms.value / prof_steps, "launches_per_step": n.value / prof_steps,
+                             "avg_launch_us": ms.value / n.value * 1e3, "bytes_per_launch": by.value / n.value,
+                             "flops_per_launch": fl.value / n.value,
+                             "achieved_GBs": by.value / ms.value / 1e6 if ms.value else 0.0,
+                             "achieved_TFLOPs": fl.value / ms.value / 1e9 if ms.value else 0.0}
+    W.lib.wisp_profile_enable(0)
+    dom = max(("gemm", "attention"), key=lambda k: classes.get(k, {}).get("ms_per_step", 0.0))
+    c = classes[dom]
+    mfma_bound = dom == "gemm" and M >= 630
+    if mfma_bound:
+        roof = {"bound": "mfma", "achieved": c["achieved_TFLOPs"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["kernel"] = "dense projections (gemm_ring_kernel / gemm_bf16_kernel)" if dom == "gemm" else "attn_bf16_kernel + attn_combine_kernel"
+    tr = traffic_from_counters(f"{dom}_{args.config}")
+    roof["traffic"] = tr
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log("copy calibration: 1 GiB device-to-device copy done")
+
+    result = {
+        "metric": "accepted tokens/s + verify-step latency (ms) vs batch B, 8B-shape bf16",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if s.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random-init weights, synthetic paged context KV, drafts from the target's own logits plus noise)",
+        "config": {"workload": f"{args.config}: {s.name} verification step", "B": mix.B, "rows": M,
+                   "sum_ctx": int(mix.ctx_len.sum()), "sum_gamma": int(mix.gamma.sum()), "page": 16,
+                   "layers": s.n_layers, "vocab": s.vocab},
+        "accepted_drafts_per_s": int(L.sum()) / (ms_step / 1e3),
+        "acceptance_rate": float(L.sum()) / max(1, int(mix.gamma.sum())),
+        "committed_tokens_per_step": committed,
+        "roofline": roof,
+        "kernels": classes,
+    }
+    if not args.no_cpu_baseline:
+        sample = int(np.argsort(mix.ctx_len)[mix.B // 2])
+        try:
+            result["cpu_baseline"] = cpu_baseline(mix, sample)
+        except MemoryError as e:   # report rather than fail the GPU measurement
+            result["cpu_baseline"] = {"value": None, "error": str(e)}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -159,7 +159,7 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
  * logits: the same kernels and random streams as wisp_verify's last stage.
  * Uses desc->B, gamma, req_id, temperature only.  logits DEVICE fp32 [M][vocab].
  */
-size_t wisp_accept_workspace_size(const wisp_batch_desc *desc);
+size_t wisp_accept_workspace_size(const wisp_batch_desc *desc, int32_t vocab);
 wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float *logits,
                         const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
                         int32_t *accept_len, int32_t *out_tokens, void *workspace,
@@ -185,6 +185,25 @@ wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint3
 /* Synchronise `stream`, then report (and clear) device-side input faults recorded in
  * `workspace` by the last wisp_verify / wisp_accept on it. */
 wisp_status wisp_check(void *workspace, void *stream);
+
+/*
+ * Opt-in timing of wisp_verify's kernels by class (instrumentation for benchmarks; off by
+ * default, process-wide, not thread-safe).  While enabled, each launch of a class is
+ * bracketed by HIP events on the caller's stream, and the class accumulates the measured
+ * milliseconds, the launch count and the algorithmic bytes / flops of its launches
+ *   GEMM: 2-byte (bf16) or 4-byte weights N*K + activations M*K, fp32 result M*N;
+ *   ATTN: K and V bytes of every token each kv head reads (ctx_len + gamma + 1 per request);
+ *   SAMPLER: two passes over the fp32 logits plus one row per request.
+ * wisp_profile_read synchronises on the recorded events.
+ */
+#define WISP_PROF_GEMM 0
+#define WISP_PROF_ATTN 1
+#define WISP_PROF_ROWS 2
+#define WISP_PROF_SAMPLER 3
+#define WISP_PROF_KINDS 4
+wisp_status wisp_profile_enable(int on);
+wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops);
+wisp_status wisp_profile_reset(void);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char *wisp_last_error(void);

@@ -35,8 +35,10 @@ def _to_storage(t: torch.Tensor, shape: wi.ModelShape) -> np.ndarray:
     return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
-def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=None):
-    """Write the input generator's synthetic context KV of the given requests into host pools."""
+def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=None, req_keys=None):
+    """Write the input generator's synthetic context KV of the given requests into host pools.
+    req_keys[i] (default i) is the request index that keys request i's generated values, so a
+    request of a large batch can be reproduced on its own."""
     s = mix.shape
     kp, vp = pools
     dt = torch.float32 if s.dtype == "f32" else torch.bfloat16
@@ -47,7 +49,8 @@ def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=Non
         if n == 0:
             continue
         for li, l in enumerate(lays):
-            K, V = wi.kv_values(mix.seed, l, i, 0, n, s.n_kv_heads, s.head_dim, "cpu", dt)
+            key = i if req_keys is None else int(req_keys[i])
+            K, V = wi.kv_values(mix.seed, l, key, 0, n, s.n_kv_heads, s.head_dim, "cpu", dt)
             Kn = _to_storage(K, s)
             Vn = _to_storage(V, s)
             kidx = wi.k_page_index(s.head_dim)

@@ -34,7 +34,8 @@ TAG_ACCEPT = 1
 TAG_RACE = 2
 
 EXPORTS = ("wisp_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
-           "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_last_error")
+           "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
+           "wisp_profile_read", "wisp_profile_reset", "wisp_last_error")
 
 
 class WispError(RuntimeError):
@@ -84,7 +85,7 @@ def _load():
     L = C.CDLL(LIB_PATH)
     L.wisp_workspace_size.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_batch_desc)]
     L.wisp_workspace_size.restype = C.c_size_t
-    L.wisp_accept_workspace_size.argtypes = [C.POINTER(wisp_batch_desc)]
+    L.wisp_accept_workspace_size.argtypes = [C.POINTER(wisp_batch_desc), C.c_int32]
     L.wisp_accept_workspace_size.restype = C.c_size_t
     L.wisp_pack_linear.argtypes = [_VP, _VP, C.c_int32, C.c_int32, C.c_int32, _VP]
     L.wisp_verify.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
@@ -95,10 +96,14 @@ def _load():
                                  _VP, _VP, _VP, C.c_size_t, _VP]
     L.wisp_uniform.argtypes = [C.c_uint64, C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint32, _VP, _VP]
     L.wisp_check.argtypes = [_VP, _VP]
+    L.wisp_profile_enable.argtypes = [C.c_int]
+    L.wisp_profile_read.argtypes = [C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64),
+                                    C.POINTER(C.c_double), C.POINTER(C.c_double)]
+    L.wisp_profile_reset.argtypes = []
     L.wisp_last_error.argtypes = []
     L.wisp_last_error.restype = C.c_char_p
     for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
-                 "wisp_check"):
+                 "wisp_check", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -262,8 +267,8 @@ def wisp_workspace_size(model: wisp_model, desc: BatchDesc) -> int:
     return int(lib.wisp_workspace_size(C.byref(model), C.byref(desc.c)))
 
 
-def wisp_accept_workspace_size(desc: BatchDesc) -> int:
-    return int(lib.wisp_accept_workspace_size(C.byref(desc.c)))
+def wisp_accept_workspace_size(desc: BatchDesc, vocab: int) -> int:
+    return int(lib.wisp_accept_workspace_size(C.byref(desc.c), vocab))
 
 
 def wisp_pack_linear(dst, src, rows: int, cols: int, dtype: int, stream=None):

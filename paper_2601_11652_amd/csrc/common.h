@@ -39,6 +39,23 @@ template <> struct Act<uint16_t> {
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte loads.  `ld16` is a plain cached load; `ld16_stream` marks data read once
+// (the weight stream) as non-temporal so it does not evict reused data from the caches.
+__device__ __forceinline__ uint4 ld16(const void *p) {
+  const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint4 ld16_stream(const void *p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+// zero unless `ok` (the load itself is issued unconditionally from a valid address)
+__device__ __forceinline__ uint4 keep_if(bool ok, uint4 v) {
+  return ok ? v : make_uint4(0, 0, 0, 0);
+}
+
 // ---------------------------------------------------------------------------------------
 // KV page layouts (one page = 16 slots x hd of one block and kv head)
 // ---------------------------------------------------------------------------------------

@@ -49,18 +49,16 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t *__restri
     for (int t = 0; t < PER_T; ++t) {
       const int c = tid + 256 * t;
       const int f = c >> 6, lc = c & 63;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (f < A_FR) {
+      if (f < A_FR) {   // compile-time per t: the stage's A pieces come first
         const int r = rb0 + f / KS, kf = kfs + f % KS;
-        if (r < MF && kf < kf1)
-          v = *reinterpret_cast<const uint4 *>(A + (((int64_t)r * KF + kf) * 64 + lc) * 8);
+        const bool ok = r < MF && kf < kf1;
+        const int rr = ok ? r : 0, kk = ok ? kf : 0;
+        pre[t] = keep_if(ok, ld16(A + (((int64_t)rr * KF + kk) * 64 + lc) * 8));
       } else {
-        const int g = f - A_FR;
-        const int n = nb0 + g / KS, kf = kfs + g % KS;
-        if (n < NF && kf < kf1)
-          v = *reinterpret_cast<const uint4 *>(W + (((int64_t)n * KF + kf) * 64 + lc) * 8);
+        const int g = f - A_FR;   // weights: clamped, unmasked (see gemm_ring_kernel)
+        const int n = min(nb0 + g / KS, NF - 1), kf = min(kfs + g % KS, kf1 - 1);
+        pre[t] = ld16_stream(W + (((int64_t)n * KF + kf) * 64 + lc) * 8);
       }
-      pre[t] = v;
     }
   };
   auto store_stage = [&](int buf) {
@@ -113,49 +111,206 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t *__restri
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Weight-streaming variant for the step's small M: each wave keeps a ring of R weight
+// fragments in flight (registers, static ring indices, so every wait is exact), consuming
+// fragment k and immediately issuing the load of fragment k + R.  Activations are staged
+// through double-buffered LDS in chunks of R 16-wide K steps.  Sized for two waves per
+// SIMD, i.e. 8 waves x R x NT KiB of weights in flight per CU.
+// Every workgroup reads the same activation matrix; to keep concurrent workgroups from
+// requesting the same cache lines at once (which serialises on a few L2 channels), each
+// workgroup walks its K chunks in a rotated order.  The order is fixed per output tile,
+// so results stay deterministic.
+// ---------------------------------------------------------------------------------------
+template <int WM, int WN, int MT, int NT, int R>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t *__restrict__ A,
+                                                           const uint16_t *__restrict__ W,
+                                                           float *__restrict__ C, int M, int N, int K,
+                                                           int ldc, int kf_per_split) {
+  constexpr int BMF = WM * MT;
+  constexpr int NTH = 64 * WM * WN;             // threads per workgroup
+  constexpr int A_FR = BMF * R;                 // A fragments per chunk
+  constexpr int A_PER_T = (A_FR * 64 + NTH - 1) / NTH;
+  __shared__ uint4 lds[2][A_FR][64];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int KF = K >> 4, NF = N >> 5;
+  const int MF = (M + 31) >> 5;
+  const int kf0 = blockIdx.z * kf_per_split;
+  const int kf1 = min(KF, kf0 + kf_per_split);
+  const int nch = (kf1 - kf0 + R - 1) / R;
+  const int rb0 = blockIdx.y * BMF;
+  const int nbw = (blockIdx.x * WN + wn) * NT;   // this wave's first weight fragment
+  const int rot = nch > 0 ? (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)nch) : 0;
+  auto chunk_k = [&](int ch) {   // first K step of the ch-th chunk in this workgroup's order
+    int c = ch + rot;
+    c = c >= nch ? c - nch : c;
+    return kf0 + c * R;
+  };
+
+  floatx16 acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // weight fragment (nb, kf) from a clamped address and never masked: K steps outside the
+  // split meet zeroed activations (0 x finite weight = 0) and columns beyond N are never
+  // stored, so no select has to wait for the load
+  auto wload = [&](int j, int kf) {
+    const int nb = min(nbw + j, NF - 1);
+    const int kq = min(kf, kf1 - 1);
+    return ld16_stream(W + (((int64_t)nb * KF + kq) * 64 + lane) * 8);
+  };
+  uint4 ring[R][NT];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, chunk_k(0) + r);
+
+  uint4 apre[A_PER_T];
+  auto aload = [&](int ch) {
+#pragma unroll
+    for (int t = 0; t < A_PER_T; ++t) {
+      const int c = tid + NTH * t;
+      const int f = min(c >> 6, A_FR - 1), lc = c & 63;
+      const int r = rb0 + f / R, kf = chunk_k(ch) + f % R;
+      const bool ok = r < MF && kf < kf1;
+      apre[t] = keep_if(ok, ld16(A + (((int64_t)(ok ? r : 0) * KF + (ok ? kf : 0)) * 64 + lc) * 8));
+    }
+  };
+  auto astore = [&](int buf) {
+#pragma unroll
+    for (int t = 0; t < A_PER_T; ++t) {
+      const int c = tid + NTH * t;
+      if (c < A_FR * 64) lds[buf][c >> 6][c & 63] = apre[t];
+    }
+  };
+
+  aload(0);
+  astore(0);
+  __syncthreads();
+  if (nch > 1) aload(1);
+  for (int ch = 0; ch < nch; ++ch) {
+    const int buf = ch & 1;
+    const int kn = chunk_k(ch + 1 < nch ? ch + 1 : ch);   // next chunk (last: a harmless reload)
+    uint4 acur[MT], anext[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) acur[i] = lds[buf][(wm * MT + i) * R][lane];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      // activations of step r+1 are read from LDS while step r's products run
+      if (r + 1 < R) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) anext[i] = lds[buf][(wm * MT + i) * R + r + 1][lane];
+      }
+      // consume ring slot r, then refill it: the slot's register is dead once the
+      // products have issued, so no copy (and no early wait) is needed
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(acur[i]), as_bf16x8(ring[r][j]),
+                                                             acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, kn + r);
+      if (r + 1 < R) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acur[i] = anext[i];
+      }
+      __builtin_amdgcn_sched_barrier(0);   // keep each refill right after its slot's use
+    }
+    if (ch + 1 < nch) astore(buf ^ 1);
+    __syncthreads();
+    if (ch + 2 < nch) aload(ch + 2);
+  }
+
+  float *Cz = C + (int64_t)blockIdx.z * M * ldc;
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int rbase = (rb0 + wm * MT + i) * 32 + 4 * (lane >> 5);
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      if (nbw + j >= NF) continue;
+      const int col = (nbw + j) * 32 + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = rbase + 8 * (e >> 2) + (e & 3);
+        if (row < M) Cz[(int64_t)row * ldc + col] = acc[i][j][e];
+      }
+    }
+  }
+}
+
 static constexpr int kKS = 4;
 
+// Launch plan.  M <= 256 (the verification step's sum(gamma+1) rows for the batch sizes
+// served here): weight-ring kernels that hold all of A per workgroup; wide outputs use
+// 64-column wave tiles (one A fragment feeds two products), narrow ones 32-column tiles
+// with a deeper ring.  K is split until about one workgroup per CU is in flight.
+// Larger M: the LDS-tiled kernel.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
-  GemmCfg c;
+  GemmCfg c{};
   const int mf = (M + 31) / 32;
-  int mt = mf <= 2 ? 1 : mf <= 4 ? 2 : mf <= 6 ? 3 : 4;
-  c.bm = 2 * mt * 32;
-  c.bn = 128;
-  const int tiles = ((N + c.bn - 1) / c.bn) * ((M + c.bm - 1) / c.bm);
   const int KF = K / 16;
-  int splits = 1;
-  if (tiles < 200) {
-    splits = (240 + tiles - 1) / tiles;
-    const int max_split = KF / (kKS * 4) > 0 ? KF / (kKS * 4) : 1;   // >= 4 stages each
-    if (splits > max_split) splits = max_split;
-    if (splits > 16) splits = 16;
-    if (splits < 1) splits = 1;
+  int tiles, R;
+  if (mf <= 8) {
+    c.kind = N >= 16384 ? 2 : 1;
+    c.mt = mf;
+    c.bm = 32 * mf;
+    c.bn = c.kind == 2 ? 256 : 128;
+    R = c.kind == 2 ? 4 : 8;
+    tiles = (N + c.bn - 1) / c.bn;
+  } else {
+    c.kind = 0;
+    c.mt = 0;
+    c.bm = 256;
+    c.bn = 128;
+    R = kKS;
+    tiles = ((N + c.bn - 1) / c.bn) * ((M + c.bm - 1) / c.bm);
   }
+  int splits = 1;
+  while (splits < 16 && tiles * splits * 2 <= 384 && KF / (splits * 2) >= 4 * R) splits *= 2;
   int kps = (KF + splits - 1) / splits;
-  kps = (kps + kKS - 1) / kKS * kKS;
-  splits = (KF + kps - 1) / kps;
-  c.splits = splits;
+  kps = (kps + R - 1) / R * R;
+  c.splits = (KF + kps - 1) / kps;
   c.kf_per_split = kps;
   return c;
 }
 
+template <int NT, int R>
+static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W, float *C, int M,
+                        int N, int K, int ldc, int kps, hipStream_t s) {
+  switch (mt) {
+#define WISP_RING_CASE(X) \
+  case X: gemm_ring_kernel<1, 4, X, NT, R><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, kps); break;
+    WISP_RING_CASE(1)
+    WISP_RING_CASE(2)
+    WISP_RING_CASE(3)
+    WISP_RING_CASE(4)
+    WISP_RING_CASE(5)
+    WISP_RING_CASE(6)
+    WISP_RING_CASE(7)
+    WISP_RING_CASE(8)
+#undef WISP_RING_CASE
+  }
+}
+
 void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
                const GemmCfg &cfg, hipStream_t s) {
-  dim3 grid((N + cfg.bn - 1) / cfg.bn, (M + cfg.bm - 1) / cfg.bm, cfg.splits);
-  switch (cfg.bm) {
-    case 64:
-      gemm_bf16_kernel<2, 2, 1, 2, kKS><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, cfg.kf_per_split);
-      break;
-    case 128:
-      gemm_bf16_kernel<2, 2, 2, 2, kKS><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, cfg.kf_per_split);
-      break;
-    case 192:
-      gemm_bf16_kernel<2, 2, 3, 2, kKS><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, cfg.kf_per_split);
-      break;
-    default:
-      gemm_bf16_kernel<2, 2, 4, 2, kKS><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, cfg.kf_per_split);
-      break;
+  if (cfg.kind == 0) {
+    dim3 grid((N + cfg.bn - 1) / cfg.bn, (M + cfg.bm - 1) / cfg.bm, cfg.splits);
+    gemm_bf16_kernel<2, 2, 4, 2, kKS><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, cfg.kf_per_split);
+    return;
   }
+  dim3 grid((N + cfg.bn - 1) / cfg.bn, 1, cfg.splits);
+  if (cfg.kind == 1)
+    launch_ring<1, 8>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+  else
+    launch_ring<2, 4>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
 }
 
 // ---------------------------------------------------------------------------------------

@@ -7,6 +7,8 @@ namespace wisp {
 
 // ----- GEMMs: C[z][M][ldc] (fp32) = A[M][K] . W[N][K]^T over the z-th K range ----------
 struct GemmCfg {
+  int kind;         // 0: LDS-tiled (any M), 1: weight ring NT=1 R=8, 2: weight ring NT=2 R=4
+  int mt;           // ring kinds: 32-row fragments of A held by every workgroup (= ceil(M/32))
   int bm, bn;       // tile rows / cols
   int splits;       // K splits (partial sums in fp32, summed in fixed order later)
   int kf_per_split; // 16-wide K fragments per split
@@ -67,9 +69,18 @@ void attention_f32(const StepDesc &d, int B, const float *q, const float *k_pool
                    hipStream_t s);
 
 // ----- acceptance ----------------------------------------------------------------------------
+struct SamplerScratch {   // carved from the workspace; sizes from sampler_chunks(V)
+  float *part_m;          // [M][CH] chunk maxima
+  int32_t *part_i;        // [M][CH] chunk argmax (greedy)
+  double *part_s;         // [M][CH] chunk sums of exponentials
+  float *race_k;          // [B][CH][2] chunk race winners (p race, residual race)
+  int32_t *race_i;        // [B][CH][2]
+  int32_t *req_R;         // [B] first rejection
+};
+int sampler_chunks(int V);
 void sampler(const StepDesc &d, int B, int M, int V, const float *logits, const int32_t *tokens,
-             const float *q, float T, uint64_t seed, float *row_m, float *row_s, int32_t *row_amax,
-             int32_t *accept_len, int32_t *out_tokens, hipStream_t s);
+             const float *q, float T, uint64_t seed, SamplerScratch sc, int32_t *accept_len,
+             int32_t *out_tokens, hipStream_t s);
 void uniform_draws(uint64_t seed, uint32_t req, uint32_t tag, uint32_t row, uint32_t n, float *out,
                    hipStream_t s);
 void clear_ints(int *p, int n, hipStream_t s);

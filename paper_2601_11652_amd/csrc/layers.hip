@@ -40,6 +40,26 @@ __device__ __forceinline__ void store8<uint16_t>(uint16_t *out, bool packed, int
   *reinterpret_cast<uint4 *>(out + o) = w;
 }
 
+// Sum of the K-split partials of 4 consecutive fp32 columns, in fixed split order.  All
+// split loads are issued before the first add so their latencies overlap.
+constexpr int kMaxSplits = 16;
+__device__ __forceinline__ float4 sum_splits4(const float *__restrict__ p, int64_t stride, int splits) {
+  float4 v[kMaxSplits];
+#pragma unroll
+  for (int z = 0; z < kMaxSplits; ++z)
+    if (z < splits) v[z] = *reinterpret_cast<const float4 *>(p + z * stride);
+  float4 a = v[0];
+#pragma unroll
+  for (int z = 1; z < kMaxSplits; ++z)
+    if (z < splits) {
+      a.x += v[z].x;
+      a.y += v[z].y;
+      a.z += v[z].z;
+      a.w += v[z].w;
+    }
+  return a;
+}
+
 // ---------------------------------------------------------------------------------------
 __global__ void rope_table_kernel(const int32_t *__restrict__ row_pos, float *__restrict__ cs, int M,
                                   int hd, float base) {
@@ -118,12 +138,15 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float *__restrict
   extern __shared__ float row[];
   const int r = blockIdx.x;
   float *hr = h + (int64_t)r * dm;
-  for (int c = threadIdx.x; c < dm; c += 256) {
-    float acc = 0.f;
-    for (int z = 0; z < splits; ++z) acc += part[((int64_t)z * M + r) * dm + c];
-    const float v = hr[c] + acc;
-    hr[c] = v;
-    row[c] = v;
+  for (int c = threadIdx.x * 4; c < dm; c += 256 * 4) {
+    const float4 acc = sum_splits4(part + (int64_t)r * dm + c, (int64_t)M * dm, splits);
+    float4 v = *reinterpret_cast<const float4 *>(hr + c);
+    v.x += acc.x;
+    v.y += acc.y;
+    v.z += acc.z;
+    v.w += acc.w;
+    *reinterpret_cast<float4 *>(hr + c) = v;
+    *reinterpret_cast<float4 *>(row + c) = v;
   }
   __syncthreads();
   norm_store_row<T>(row, gain, xn, packed, r, dm, eps, sh);
@@ -144,26 +167,24 @@ __global__ __launch_bounds__(256) void qkv_rope_append_kernel(StepDesc d, const 
                                                               T *__restrict__ q, T *__restrict__ k_pool,
                                                               T *__restrict__ v_pool, int M, int nq,
                                                               int nkv, int hd) {
+  extern __shared__ float row[];   // the row's summed q|k|v projections
   const int r = blockIdx.x;
   const int N = (nq + 2 * nkv) * hd;
   const int h2 = hd / 2;
-  const float *pr = part + (int64_t)r * N;
-  auto val = [&](int c) {
-    float a = 0.f;
-    for (int z = 0; z < splits; ++z) a += pr[(int64_t)z * M * N + c];
-    return a;
-  };
+  for (int c = threadIdx.x * 4; c < N; c += 256 * 4)
+    *reinterpret_cast<float4 *>(row + c) = sum_splits4(part + (int64_t)r * N + c, (int64_t)M * N, splits);
+  __syncthreads();
   const int req = d.row_req[r], pos = d.row_pos[r];
-  int blk = d.page_table[(int64_t)req * d.pt_stride + pos / kPage];
+  const int blk = d.page_table[(int64_t)req * d.pt_stride + pos / kPage];
   const bool blk_ok = blk >= 0 && blk < d.n_blocks;
   if (!blk_ok && threadIdx.x == 0) flag_error(d.err, kErrBlock);
   const int slot = pos % kPage;
   const int page_elems = kPage * hd;
   const float *csr = cs + (int64_t)r * hd;   // [h2][2]
-  // rotated pairs: q heads then k heads
+  // rotated pairs (i, i + hd/2): q heads then k heads
   for (int p = threadIdx.x; p < (nq + nkv) * h2; p += 256) {
     const int head = p / h2, i = p % h2;
-    const float x1 = val(head * hd + i), x2 = val(head * hd + i + h2);
+    const float x1 = row[head * hd + i], x2 = row[head * hd + i + h2];
     const float c = csr[2 * i], sn = csr[2 * i + 1];
     const float y1 = x1 * c - x2 * sn;
     const float y2 = x2 * c + x1 * sn;
@@ -181,7 +202,7 @@ __global__ __launch_bounds__(256) void qkv_rope_append_kernel(StepDesc d, const 
     for (int e = threadIdx.x; e < nkv * hd; e += 256) {
       const int kh = e / hd, dim = e % hd;
       T *pg = v_pool + ((int64_t)blk * nkv + kh) * page_elems;
-      Act<T>::store(pg, v_page_off(slot, dim), val((nq + nkv) * hd + e));
+      Act<T>::store(pg, v_page_off(slot, dim), row[(nq + nkv) * hd + e]);
     }
   }
 }
@@ -189,7 +210,8 @@ __global__ __launch_bounds__(256) void qkv_rope_append_kernel(StepDesc d, const 
 template <typename T>
 void qkv_rope_append(const StepDesc &d, const float *part, int splits, const float *cs, T *q,
                      T *k_pool, T *v_pool, int M, int nq, int nkv, int hd, hipStream_t s) {
-  qkv_rope_append_kernel<T><<<M, 256, 0, s>>>(d, part, splits, cs, q, k_pool, v_pool, M, nq, nkv, hd);
+  const int N = (nq + 2 * nkv) * hd;
+  qkv_rope_append_kernel<T><<<M, 256, N * sizeof(float), s>>>(d, part, splits, cs, q, k_pool, v_pool, M, nq, nkv, hd);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -199,20 +221,21 @@ template <typename T>
 __global__ __launch_bounds__(256) void swiglu_kernel(const float *__restrict__ part, int splits,
                                                      T *__restrict__ out, bool packed, int M, int F) {
   const int64_t chunks = (int64_t)M * (F / 8);
+  const int64_t stride = (int64_t)M * 2 * F;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < chunks;
        t += (int64_t)gridDim.x * blockDim.x) {
     const int64_t r = t / (F / 8), c = (t % (F / 8)) * 8;
+    const float *pr = part + r * 2 * F;
+    float4 g[2], u[2];
+    g[0] = sum_splits4(pr + c, stride, splits);
+    g[1] = sum_splits4(pr + c + 4, stride, splits);
+    u[0] = sum_splits4(pr + F + c, stride, splits);
+    u[1] = sum_splits4(pr + F + c + 4, stride, splits);
+    const float gv[8] = {g[0].x, g[0].y, g[0].z, g[0].w, g[1].x, g[1].y, g[1].z, g[1].w};
+    const float uv[8] = {u[0].x, u[0].y, u[0].z, u[0].w, u[1].x, u[1].y, u[1].z, u[1].w};
     float v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float g = 0.f, u = 0.f;
-      for (int z = 0; z < splits; ++z) {
-        const float *pz = part + ((int64_t)z * M + r) * 2 * F;
-        g += pz[c + e];
-        u += pz[F + c + e];
-      }
-      v[e] = g / (1.0f + expf(-g)) * u;
-    }
+    for (int e = 0; e < 8; ++e) v[e] = gv[e] / (1.0f + expf(-gv[e])) * uv[e];
     store8<T>(out, packed, r, c, F, v);
   }
 }

@@ -33,91 +33,133 @@ __device__ __forceinline__ V block_reduce(V v, V *sh, F op) {
 }
 
 // ---------------------------------------------------------------------------------------
-// row statistics: m = max z, S = sum exp(z - m) (fp64 accumulation, rounded to fp32),
-// and the first argmax of the logits (greedy decoding)
+// The vocabulary is cut into chunks of kVChunk entries, one workgroup per (row or request,
+// chunk).  Partial results are combined in fixed chunk order.
 // ---------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void row_stats_kernel(const float *__restrict__ logits, int V,
-                                                        float T, float *__restrict__ row_m,
-                                                        float *__restrict__ row_s,
-                                                        int32_t *__restrict__ row_amax) {
-  __shared__ float shf[4];
-  __shared__ double shd[4];
-  __shared__ float shv[4];
-  __shared__ int shi[4];
-  const int64_t r = blockIdx.x;
-  const float *l = logits + r * V;
-  if (T == 0.f) {
-    float bv = -INFINITY;
-    int bi = 0x7FFFFFFF;
-    for (int k = threadIdx.x; k < V; k += 256) {
-      const float v = l[k];
-      if (v > bv) {
-        bv = v;
-        bi = k;
-      }
-    }
-    // (value, index) reduction: larger value wins, smaller index on ties
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o);
-      const int oi = __shfl_xor(bi, o);
-      if (ov > bv || (ov == bv && oi < bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
-    if ((threadIdx.x & 63) == 0) {
-      shv[threadIdx.x >> 6] = bv;
-      shi[threadIdx.x >> 6] = bi;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      bv = shv[0];
-      bi = shi[0];
-      for (int w = 1; w < 4; ++w)
-        if (shv[w] > bv || (shv[w] == bv && shi[w] < bi)) {
-          bv = shv[w];
-          bi = shi[w];
-        }
-      row_amax[r] = bi;
-      row_m[r] = bv;
-      row_s[r] = 1.f;
-    }
-    return;
-  }
-  float mx = -INFINITY;
-  for (int k = threadIdx.x; k < V; k += 256) mx = fmaxf(mx, l[k] / T);
-  mx = block_reduce(mx, shf, [](float a, float b) { return fmaxf(a, b); });
-  double sum = 0.0;
-  for (int k = threadIdx.x; k < V; k += 256) sum += (double)expf(l[k] / T - mx);
-  sum = block_reduce(sum, shd, [](double a, double b) { return a + b; });
-  if (threadIdx.x == 0) {
-    row_m[r] = mx;
-    row_s[r] = (float)sum;
-    row_amax[r] = -1;
-  }
-}
+constexpr int kVChunk = 8192;
 
-// ---------------------------------------------------------------------------------------
-// accept scan + extra-token race, one workgroup per request
-// ---------------------------------------------------------------------------------------
 __device__ __forceinline__ bool better(float ka, int ia, float kb, int ib) {
   return ka > kb || (ka == kb && ia < ib);
 }
 
-__global__ __launch_bounds__(256) void accept_kernel(StepDesc d, int V, const float *__restrict__ logits,
-                                                     const int32_t *__restrict__ tokens,
-                                                     const float *__restrict__ q, float T,
-                                                     uint64_t seed, const float *__restrict__ row_m,
-                                                     const float *__restrict__ row_s,
-                                                     const int32_t *__restrict__ row_amax,
-                                                     int32_t *__restrict__ accept_len,
-                                                     int32_t *__restrict__ out_tokens) {
+// (key, index) argmax across the 256 threads; ties go to the smaller index
+__device__ __forceinline__ void block_argmax(float &k, int &i, float *shk, int *shi) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ok = __shfl_xor(k, o);
+    const int oi = __shfl_xor(i, o);
+    if (better(ok, oi, k, i)) {
+      k = ok;
+      i = oi;
+    }
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    shk[threadIdx.x >> 6] = k;
+    shi[threadIdx.x >> 6] = i;
+  }
+  __syncthreads();
+  k = shk[0];
+  i = shi[0];
+  for (int w = 1; w < 4; ++w)
+    if (better(shk[w], shi[w], k, i)) {
+      k = shk[w];
+      i = shi[w];
+    }
+}
+
+// pass 1: per chunk, max of z = l / T (T > 0) or (max, first argmax) of l (T == 0)
+__global__ __launch_bounds__(256) void row_max_kernel(const float *__restrict__ logits, int V, float T,
+                                                      int CH, float *__restrict__ part_m,
+                                                      int32_t *__restrict__ part_i) {
+  __shared__ float shk[4];
+  __shared__ int shi[4];
+  const int c = blockIdx.y;
+  const int64_t r = blockIdx.x;
+  const float *l = logits + r * V;
+  const int k1 = min(V, (c + 1) * kVChunk);
+  float bk = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int k = c * kVChunk + threadIdx.x; k < k1; k += 256) {
+    const float z = T == 0.f ? l[k] : l[k] / T;
+    if (z > bk) {
+      bk = z;
+      bi = k;
+    }
+  }
+  block_argmax(bk, bi, shk, shi);
+  if (threadIdx.x == 0) {
+    part_m[r * CH + c] = bk;
+    part_i[r * CH + c] = bi;
+  }
+}
+
+__device__ __forceinline__ float row_max_of(const float *part_m, int64_t r, int CH) {
+  float m = part_m[r * CH];
+  for (int c = 1; c < CH; ++c) m = fmaxf(m, part_m[r * CH + c]);
+  return m;
+}
+
+// pass 2: per chunk, sum of exp(z - m) in fp64 (m = the row's max)
+__global__ __launch_bounds__(256) void row_sum_kernel(const float *__restrict__ logits, int V, float T,
+                                                      int CH, const float *__restrict__ part_m,
+                                                      double *__restrict__ part_s) {
+  __shared__ double shd[4];
+  const int c = blockIdx.y;
+  const int64_t r = blockIdx.x;
+  const float *l = logits + r * V;
+  const float m = row_max_of(part_m, r, CH);
+  const int k1 = min(V, (c + 1) * kVChunk);
+  double sum = 0.0;
+  for (int k = c * kVChunk + threadIdx.x; k < k1; k += 256) sum += (double)expf(l[k] / T - m);
+  sum = block_reduce(sum, shd, [](double a, double b) { return a + b; });
+  if (threadIdx.x == 0) part_s[r * CH + c] = sum;
+}
+
+struct RowStat {
+  float m, S;
+  int amax;
+};
+
+__device__ RowStat row_stat(const float *part_m, const int32_t *part_i, const double *part_s, int64_t r,
+                            int CH, float T) {
+  RowStat st;
+  if (T == 0.f) {
+    float bk = part_m[r * CH];
+    int bi = part_i[r * CH];
+    for (int c = 1; c < CH; ++c)
+      if (better(part_m[r * CH + c], part_i[r * CH + c], bk, bi)) {
+        bk = part_m[r * CH + c];
+        bi = part_i[r * CH + c];
+      }
+    st.m = bk;
+    st.S = 1.f;
+    st.amax = bi;
+    return st;
+  }
+  st.m = row_max_of(part_m, r, CH);
+  double s = 0.0;
+  for (int c = 0; c < CH; ++c) s += part_s[r * CH + c];
+  st.S = (float)s;
+  st.amax = -1;
+  return st;
+}
+
+// pass 3: Eq. (1)-(2) accept scan (recomputed by every chunk's workgroup, <= 16 steps),
+// then that chunk's part of the exponential race for the extra token (Eq. (3) / residual)
+__global__ __launch_bounds__(256) void race_kernel(StepDesc d, int V, const float *__restrict__ logits,
+                                                   const int32_t *__restrict__ tokens,
+                                                   const float *__restrict__ q, float T, uint64_t seed,
+                                                   int CH, const float *__restrict__ part_m,
+                                                   const int32_t *__restrict__ part_i,
+                                                   const double *__restrict__ part_s,
+                                                   float *__restrict__ race_k, int32_t *__restrict__ race_i,
+                                                   int32_t *__restrict__ req_R) {
   __shared__ int R_sh;
-  __shared__ float shk[2][4];
-  __shared__ int shi[2][4];
+  __shared__ float shk[4];
+  __shared__ int shi[4];
   __shared__ int shany[4];
-  const int i = blockIdx.x;
+  const int c = blockIdx.y, i = blockIdx.x;
   const int gam = d.gamma[i], off = d.off[i], doff = d.doff[i];
   const uint32_t req = d.req_id[i];
   if (threadIdx.x == 0) {
@@ -125,17 +167,18 @@ __global__ __launch_bounds__(256) void accept_kernel(StepDesc d, int V, const fl
     for (int j = 1; j <= gam; ++j) {
       int y = tokens[off + j];
       if (y < 0 || y >= V) {
-        flag_error(d.err, kErrToken);
+        if (c == 0) flag_error(d.err, kErrToken);
         y = 0;
       }
       const int64_t pr = off + j - 1;
+      const RowStat st = row_stat(part_m, part_i, part_s, pr, CH, T);
       if (T == 0.f) {
-        if (y != row_amax[pr]) {
+        if (y != st.amax) {
           R = j;
           break;
         }
       } else {
-        const float P = expf(logits[pr * V + y] / T - row_m[pr]) / row_s[pr];
+        const float P = expf(logits[pr * V + y] / T - st.m) / st.S;
         const float Q = q[(int64_t)(doff + j - 1) * V + y];
         const float a = Q > 0.f ? fminf(1.f, P / Q) : (P > 0.f ? 1.f : 0.f);
         const float u = uniform_from_word(draw(seed, 0u, (uint32_t)j, req, kTagAccept).v[0]);
@@ -146,112 +189,108 @@ __global__ __launch_bounds__(256) void accept_kernel(StepDesc d, int V, const fl
       }
     }
     R_sh = R;
+    if (c == 0) req_R[i] = R;
   }
   __syncthreads();
-  const int R = R_sh, L = R - 1, r = R - 1;
+  if (T == 0.f) return;
+  const int R = R_sh, r = R - 1;
   const int64_t lr = off + r;
-  int extra;
-  if (T == 0.f) {
-    extra = row_amax[lr];
-  } else {
-    const float *l = logits + lr * V;
-    const bool rejected = R <= gam;
-    const float *qr = q + (int64_t)(doff + (rejected ? R - 1 : 0)) * V;
-    const float m = row_m[lr], S = row_s[lr];
-    float kR = -INFINITY, kP = -INFINITY;
-    int iR = 0x7FFFFFFF, iP = 0x7FFFFFFF;
-    int any = 0;
-    for (int k4 = threadIdx.x; k4 * 4 < V; k4 += 256) {
-      const Philox4 w = draw(seed, (uint32_t)k4, (uint32_t)r, req, kTagRace);
+  const float *l = logits + lr * V;
+  const bool rejected = R <= gam;
+  const float *qr = q + (int64_t)(doff + (rejected ? R - 1 : 0)) * V;
+  const RowStat st = row_stat(part_m, part_i, part_s, lr, CH, T);
+  float kR = -INFINITY, kP = -INFINITY;
+  int iR = 0x7FFFFFFF, iP = 0x7FFFFFFF;
+  int any = 0;
+  const int k4_0 = c * (kVChunk / 4), k4_1 = min((V + 3) / 4, (c + 1) * (kVChunk / 4));
+  for (int k4 = k4_0 + threadIdx.x; k4 < k4_1; k4 += 256) {
+    const Philox4 w = draw(seed, (uint32_t)k4, (uint32_t)r, req, kTagRace);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int k = k4 * 4 + e;
-        if (k >= V) break;
-        const float z = l[k] / T;
-        const float g = logf(-logf(uniform_from_word(w.v[e])));
-        const float keyp = z - g;
-        if (keyp > kP) {
-          kP = keyp;
-          iP = k;
-        }
-        if (rejected) {
-          const float p = expf(z - m) / S;
-          const float wk = p - qr[k];
-          if (wk > 0.f) {
-            any = 1;
-            const float keyr = logf(wk) - g;
-            if (keyr > kR) {
-              kR = keyr;
-              iR = k;
-            }
+    for (int e = 0; e < 4; ++e) {
+      const int k = k4 * 4 + e;
+      if (k >= V) break;
+      const float z = l[k] / T;
+      const float g = logf(-logf(uniform_from_word(w.v[e])));
+      const float keyp = z - g;
+      if (keyp > kP) {
+        kP = keyp;
+        iP = k;
+      }
+      if (rejected) {
+        const float wk = expf(z - st.m) / st.S - qr[k];
+        if (wk > 0.f) {
+          any = 1;
+          const float keyr = logf(wk) - g;
+          if (keyr > kR) {
+            kR = keyr;
+            iR = k;
           }
         }
       }
     }
-    // per-thread candidates were visited in ascending k, so strict '>' kept the first
+  }
+  block_argmax(kP, iP, shk, shi);
+  block_argmax(kR, iR, shk, shi);
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      float ok = __shfl_xor(kP, o);
-      int oi = __shfl_xor(iP, o);
-      if (better(ok, oi, kP, iP)) {
-        kP = ok;
-        iP = oi;
-      }
-      ok = __shfl_xor(kR, o);
-      oi = __shfl_xor(iR, o);
-      if (better(ok, oi, kR, iR)) {
-        kR = ok;
-        iR = oi;
-      }
-      any |= __shfl_xor(any, o);
-    }
-    const int w = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-      shk[0][w] = kP;
-      shi[0][w] = iP;
-      shk[1][w] = kR;
-      shi[1][w] = iR;
-      shany[w] = any;
-    }
-    __syncthreads();
-    kP = shk[0][0];
-    iP = shi[0][0];
-    kR = shk[1][0];
-    iR = shi[1][0];
-    any = shany[0];
-    for (int v = 1; v < 4; ++v) {
-      if (better(shk[0][v], shi[0][v], kP, iP)) {
-        kP = shk[0][v];
-        iP = shi[0][v];
-      }
-      if (better(shk[1][v], shi[1][v], kR, iR)) {
-        kR = shk[1][v];
-        iR = shi[1][v];
-      }
-      any |= shany[v];
-    }
-    extra = (rejected && any) ? iR : iP;
+  for (int o = 32; o > 0; o >>= 1) any |= __shfl_xor(any, o);
+  if ((threadIdx.x & 63) == 0) shany[threadIdx.x >> 6] = any;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    any = shany[0] | shany[1] | shany[2] | shany[3];
+    const int64_t o = ((int64_t)i * CH + c) * 2;
+    race_k[o] = kP;
+    race_i[o] = iP;
+    race_k[o + 1] = any ? kR : -INFINITY;
+    race_i[o + 1] = any ? iR : 0x7FFFFFFF;
   }
-  for (int j = threadIdx.x; j <= gam; j += 256) {
-    int v;
-    if (j < L)
-      v = tokens[off + j + 1];
-    else if (j == L)
-      v = extra;
-    else
-      v = -1;
-    out_tokens[off + j] = v;
-  }
-  if (threadIdx.x == 0) accept_len[i] = L;
 }
 
+// pass 4: combine the chunks' race winners in fixed order, write the outputs
+__global__ void finalize_kernel(StepDesc d, int B, const int32_t *__restrict__ tokens, float T, int CH,
+                                const float *__restrict__ part_m, const int32_t *__restrict__ part_i,
+                                const double *__restrict__ part_s, const float *__restrict__ race_k,
+                                const int32_t *__restrict__ race_i, const int32_t *__restrict__ req_R,
+                                int32_t *__restrict__ accept_len, int32_t *__restrict__ out_tokens) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B) return;
+  const int gam = d.gamma[i], off = d.off[i];
+  const int R = req_R[i], L = R - 1;
+  int extra;
+  if (T == 0.f) {
+    extra = row_stat(part_m, part_i, part_s, off + R - 1, CH, T).amax;
+  } else {
+    float kP = -INFINITY, kR = -INFINITY;
+    int iP = 0x7FFFFFFF, iR = 0x7FFFFFFF;
+    for (int c = 0; c < CH; ++c) {
+      const int64_t o = ((int64_t)i * CH + c) * 2;
+      if (better(race_k[o], race_i[o], kP, iP)) {
+        kP = race_k[o];
+        iP = race_i[o];
+      }
+      if (race_i[o + 1] != 0x7FFFFFFF && better(race_k[o + 1], race_i[o + 1], kR, iR)) {
+        kR = race_k[o + 1];
+        iR = race_i[o + 1];
+      }
+    }
+    extra = (R <= gam && iR != 0x7FFFFFFF) ? iR : iP;
+  }
+  for (int j = 0; j <= gam; ++j) out_tokens[off + j] = j < L ? tokens[off + j + 1] : (j == L ? extra : -1);
+  accept_len[i] = L;
+}
+
+int sampler_chunks(int V) { return (V + kVChunk - 1) / kVChunk; }
+
 void sampler(const StepDesc &d, int B, int M, int V, const float *logits, const int32_t *tokens,
-             const float *q, float T, uint64_t seed, float *row_m, float *row_s, int32_t *row_amax,
-             int32_t *accept_len, int32_t *out_tokens, hipStream_t s) {
-  if (M > 0) row_stats_kernel<<<M, 256, 0, s>>>(logits, V, T, row_m, row_s, row_amax);
-  if (B > 0)
-    accept_kernel<<<B, 256, 0, s>>>(d, V, logits, tokens, q, T, seed, row_m, row_s, row_amax,
-                                    accept_len, out_tokens);
+             const float *q, float T, uint64_t seed, SamplerScratch sc, int32_t *accept_len,
+             int32_t *out_tokens, hipStream_t s) {
+  if (B == 0) return;
+  const int CH = sampler_chunks(V);
+  row_max_kernel<<<dim3(M, CH), 256, 0, s>>>(logits, V, T, CH, sc.part_m, sc.part_i);
+  if (T != 0.f) row_sum_kernel<<<dim3(M, CH), 256, 0, s>>>(logits, V, T, CH, sc.part_m, sc.part_s);
+  race_kernel<<<dim3(B, CH), 256, 0, s>>>(d, V, logits, tokens, q, T, seed, CH, sc.part_m, sc.part_i,
+                                          sc.part_s, sc.race_k, sc.race_i, sc.req_R);
+  finalize_kernel<<<(B + 63) / 64, 64, 0, s>>>(d, B, tokens, T, CH, sc.part_m, sc.part_i, sc.part_s,
+                                               sc.race_k, sc.race_i, sc.req_R, accept_len, out_tokens);
 }
 
 __global__ void uniform_kernel(uint64_t seed, uint32_t req, uint32_t tag, uint32_t row, uint32_t n,

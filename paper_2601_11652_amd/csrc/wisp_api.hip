@@ -51,7 +51,8 @@ struct Plan {
          i_items = 0, i_groups = 0;
   // byte offsets inside the workspace
   size_t w_err = 0, w_desc = 0, w_rope = 0, w_h = 0, w_xn = 0, w_ao = 0, w_af = 0, w_q = 0,
-         w_part = 0, w_attn_o = 0, w_attn_ml = 0, w_m = 0, w_s = 0, w_amax = 0, total = 0;
+         w_part = 0, w_attn_o = 0, w_attn_ml = 0, w_sm = 0, w_si = 0, w_ss = 0, w_rk = 0, w_ri = 0,
+         w_rR = 0, total = 0;
 };
 
 constexpr int kAttnTargetItems = 1024;
@@ -107,9 +108,10 @@ void carve(Plan &p, size_t &w, size_t &field, size_t bytes) {
   w = align256(w + bytes);
 }
 
-// forward=true: the full step; false: acceptance only (rows/drafts of the batch)
-void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward) {
+// forward=true: the full step; false: acceptance only (rows/drafts of the batch, vocab V)
+void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward, int vocab = 0) {
   p.B = d->B;
+  p.V = forward ? m->vocab : vocab;
   std::vector<int> off(p.B + 1, 0), doff(p.B + 1, 0);
   for (int i = 0; i < p.B; ++i) {
     off[i + 1] = off[i] + d->gamma[i] + 1;
@@ -209,9 +211,13 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
   size_t w = 0;
   carve(p, w, p.w_err, 256);
   carve(p, w, p.w_desc, p.host.size() * sizeof(int32_t));
-  carve(p, w, p.w_m, (size_t)p.M * 4);
-  carve(p, w, p.w_s, (size_t)p.M * 4);
-  carve(p, w, p.w_amax, (size_t)p.M * 4);
+  const int CH = sampler_chunks(std::max(p.V, 1));
+  carve(p, w, p.w_sm, (size_t)p.M * CH * 4);
+  carve(p, w, p.w_si, (size_t)p.M * CH * 4);
+  carve(p, w, p.w_ss, (size_t)p.M * CH * 8);
+  carve(p, w, p.w_rk, (size_t)p.B * CH * 2 * 4);
+  carve(p, w, p.w_ri, (size_t)p.B * CH * 2 * 4);
+  carve(p, w, p.w_rR, (size_t)p.B * 4);
   if (forward) {
     const size_t es = p.bf16 ? 2 : 4;
     carve(p, w, p.w_rope, (size_t)p.M * p.hd * 4);
@@ -232,6 +238,69 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
     carve(p, w, p.w_attn_ml, p.items.size() * 64 * 2 * 4);
   }
   p.total = w;
+}
+
+// ------------------------------------------------------------------------------------------
+// optional per-kernel-class timing (HIP events around each launch on the caller's stream)
+// ------------------------------------------------------------------------------------------
+struct ProfRec {
+  int kind;
+  double bytes, flops;
+  hipEvent_t a, b;
+};
+struct ProfState {
+  bool on = false;
+  std::vector<ProfRec> pending;
+  std::vector<hipEvent_t> free_events;
+  double ms[WISP_PROF_KINDS] = {}, bytes[WISP_PROF_KINDS] = {}, flops[WISP_PROF_KINDS] = {};
+  int64_t launches[WISP_PROF_KINDS] = {};
+};
+ProfState g_prof;
+
+hipEvent_t prof_event() {
+  if (!g_prof.free_events.empty()) {
+    hipEvent_t e = g_prof.free_events.back();
+    g_prof.free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+
+struct ProfScope {   // records [begin, end) of one launch when profiling is on
+  int kind;
+  double bytes, flops;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  ProfScope(int k, double by, double fl, hipStream_t st) : kind(k), bytes(by), flops(fl), s(st) {
+    if (g_prof.on) {
+      a = prof_event();
+      (void)hipEventRecord(a, s);
+    }
+  }
+  ~ProfScope() {
+    if (a) {
+      hipEvent_t b = prof_event();
+      (void)hipEventRecord(b, s);
+      g_prof.pending.push_back({kind, bytes, flops, a, b});
+    }
+  }
+};
+
+void prof_collect() {
+  for (auto &r : g_prof.pending) {
+    (void)hipEventSynchronize(r.b);
+    float ms = 0.f;
+    (void)hipEventElapsedTime(&ms, r.a, r.b);
+    g_prof.ms[r.kind] += ms;
+    g_prof.bytes[r.kind] += r.bytes;
+    g_prof.flops[r.kind] += r.flops;
+    g_prof.launches[r.kind] += 1;
+    g_prof.free_events.push_back(r.a);
+    g_prof.free_events.push_back(r.b);
+  }
+  g_prof.pending.clear();
 }
 
 // pinned staging for the descriptor upload, reused once the previous copy has finished
@@ -267,6 +336,17 @@ wisp_status upload(const Plan &p, char *ws, hipStream_t s) {
   if (hipEventRecord(g_stage.ev, s) != hipSuccess) return fail(WISP_E_HIP, "event record failed");
   g_stage.pending = true;
   return WISP_OK;
+}
+
+SamplerScratch sampler_scratch(const Plan &p, char *ws) {
+  SamplerScratch sc;
+  sc.part_m = reinterpret_cast<float *>(ws + p.w_sm);
+  sc.part_i = reinterpret_cast<int32_t *>(ws + p.w_si);
+  sc.part_s = reinterpret_cast<double *>(ws + p.w_ss);
+  sc.race_k = reinterpret_cast<float *>(ws + p.w_rk);
+  sc.race_i = reinterpret_cast<int32_t *>(ws + p.w_ri);
+  sc.req_R = reinterpret_cast<int32_t *>(ws + p.w_rR);
+  return sc;
 }
 
 StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_blocks) {
@@ -307,53 +387,77 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
   const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
   const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
 
-  rope_table(sd, cs, p.M, p.hd, m->rope_base, s);
-  embed_norm<T>(sd, (const T *)m->embed, (const T *)m->attn_norm[0], tokens, h, xn, packed, p.M, p.d,
-                p.V, m->rms_eps, s);
+  const double es = p.bf16 ? 2.0 : 4.0;
+  auto gemm_bytes = [&](int N, int K) { return es * ((double)N * K + (double)p.M * K) + 4.0 * p.M * N; };
+  auto gemm_flops = [&](int N, int K) { return 2.0 * p.M * N * K; };
+  const double kv_tok = 2.0 * p.nkv * p.hd * es;   // K and V bytes per token per layer
+  double attn_bytes = 0.0, attn_flops = 0.0;
+  for (const AttnItem &it : p.items) {
+    const int G = p.G;
+    const int rows = (int)p.host[p.i_gamma + it.req] + 1;
+    const int rbg = it.kvh_rbg >> 16;
+    const int nr = std::min(64, rows * G - rbg * 64);
+    if (rbg == 0) attn_bytes += (double)(it.t1 - it.t0) * kv_tok / p.nkv;
+    attn_flops += 4.0 * p.hd * nr * (it.t1 - it.t0);
+  }
+  {
+    ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
+    rope_table(sd, cs, p.M, p.hd, m->rope_base, s);
+    embed_norm<T>(sd, (const T *)m->embed, (const T *)m->attn_norm[0], tokens, h, xn, packed, p.M, p.d,
+                  p.V, m->rms_eps, s);
+  }
   for (int l = 0; l < m->n_layers; ++l) {
     T *kl = (T *)kv->k_pool + l * layer_elems;
     T *vl = (T *)kv->v_pool + l * layer_elems;
-    int sq = 1, so = 1, sg = 1, sdn = 1;
-    if (p.bf16) {
-      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->w_qkv[l], part, p.M, p.qkvN, p.d, p.qkvN, p.g_qkv, s);
-      sq = p.g_qkv.splits;
-    } else {
-      gemm_f32((const float *)xn, (const float *)m->w_qkv[l], part, p.M, p.qkvN, p.d, p.qkvN, s);
+    // one dense projection: C = act . W^T (fp32 partials over cfg.splits K ranges)
+    auto gemm = [&](const T *act, const void *w, float *out, int N, int K, const GemmCfg &cfg) {
+      ProfScope ps(WISP_PROF_GEMM, gemm_bytes(N, K), gemm_flops(N, K), s);
+      if (p.bf16)
+        gemm_bf16((const uint16_t *)act, (const uint16_t *)w, out, p.M, N, K, N, cfg, s);
+      else
+        gemm_f32((const float *)act, (const float *)w, out, p.M, N, K, N, s);
+      return p.bf16 ? cfg.splits : 1;
+    };
+    const int sq = gemm(xn, m->w_qkv[l], part, p.qkvN, p.d, p.g_qkv);
+    {
+      ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
+      qkv_rope_append<T>(sd, part, sq, cs, qb, kl, vl, p.M, p.nq, p.nkv, p.hd, s);
     }
-    qkv_rope_append<T>(sd, part, sq, cs, qb, kl, vl, p.M, p.nq, p.nkv, p.hd, s);
-    if (p.bf16) {
-      attention_bf16(sd, items, (int)p.items.size(), groups, (int)p.groups.size(), (const uint16_t *)qb,
-                     (const uint16_t *)kl, (const uint16_t *)vl, reinterpret_cast<float *>(ws + p.w_attn_o),
-                     reinterpret_cast<float *>(ws + p.w_attn_ml), (uint16_t *)ao, true, p.qdim, p.nq,
-                     p.nkv, p.hd, s);
-      gemm_bf16((const uint16_t *)ao, (const uint16_t *)m->w_o[l], part, p.M, p.d, p.qdim, p.d, p.g_o, s);
-      so = p.g_o.splits;
-    } else {
-      attention_f32(sd, p.B, (const float *)qb, (const float *)kl, (const float *)vl, (float *)ao, p.nq,
-                    p.nkv, p.hd, p.max_tokens, s);
-      gemm_f32((const float *)ao, (const float *)m->w_o[l], part, p.M, p.d, p.qdim, p.d, s);
+    {
+      ProfScope ps(WISP_PROF_ATTN, attn_bytes, attn_flops, s);
+      if (p.bf16)
+        attention_bf16(sd, items, (int)p.items.size(), groups, (int)p.groups.size(), (const uint16_t *)qb,
+                       (const uint16_t *)kl, (const uint16_t *)vl, reinterpret_cast<float *>(ws + p.w_attn_o),
+                       reinterpret_cast<float *>(ws + p.w_attn_ml), (uint16_t *)ao, true, p.qdim, p.nq,
+                       p.nkv, p.hd, s);
+      else
+        attention_f32(sd, p.B, (const float *)qb, (const float *)kl, (const float *)vl, (float *)ao, p.nq,
+                      p.nkv, p.hd, p.max_tokens, s);
     }
-    resid_norm<T>(part, so, h, (const T *)m->mlp_norm[l], xn, packed, p.M, p.d, m->rms_eps, s);
-    if (p.bf16) {
-      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->w_gate_up[l], part, p.M, 2 * p.F, p.d, 2 * p.F, p.g_gu, s);
-      sg = p.g_gu.splits;
-    } else {
-      gemm_f32((const float *)xn, (const float *)m->w_gate_up[l], part, p.M, 2 * p.F, p.d, 2 * p.F, s);
+    const int so = gemm(ao, m->w_o[l], part, p.d, p.qdim, p.g_o);
+    {
+      ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
+      resid_norm<T>(part, so, h, (const T *)m->mlp_norm[l], xn, packed, p.M, p.d, m->rms_eps, s);
     }
-    swiglu<T>(part, sg, af, packed, p.M, p.F, s);
-    if (p.bf16) {
-      gemm_bf16((const uint16_t *)af, (const uint16_t *)m->w_down[l], part, p.M, p.d, p.F, p.d, p.g_down, s);
-      sdn = p.g_down.splits;
-    } else {
-      gemm_f32((const float *)af, (const float *)m->w_down[l], part, p.M, p.d, p.F, p.d, s);
+    const int sg = gemm(xn, m->w_gate_up[l], part, 2 * p.F, p.d, p.g_gu);
+    {
+      ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
+      swiglu<T>(part, sg, af, packed, p.M, p.F, s);
     }
+    const int sdn = gemm(af, m->w_down[l], part, p.d, p.F, p.g_down);
     const T *gain = (l + 1 < m->n_layers) ? (const T *)m->attn_norm[l + 1] : (const T *)m->final_norm;
-    resid_norm<T>(part, sdn, h, gain, xn, packed, p.M, p.d, m->rms_eps, s);
+    {
+      ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
+      resid_norm<T>(part, sdn, h, gain, xn, packed, p.M, p.d, m->rms_eps, s);
+    }
   }
-  if (p.bf16)
-    gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.M, p.V, p.d, p.V, p.g_lm, s);
-  else
-    gemm_f32((const float *)xn, (const float *)m->lm_head, logits, p.M, p.V, p.d, p.V, s);
+  {
+    ProfScope ps(WISP_PROF_GEMM, gemm_bytes(p.V, p.d), gemm_flops(p.V, p.d), s);
+    if (p.bf16)
+      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.M, p.V, p.d, p.V, p.g_lm, s);
+    else
+      gemm_f32((const float *)xn, (const float *)m->lm_head, logits, p.M, p.V, p.d, p.V, s);
+  }
   return hip_check("forward launch");
 }
 
@@ -373,10 +477,10 @@ size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc)
   return p.total;
 }
 
-size_t wisp_accept_workspace_size(const wisp_batch_desc *desc) {
-  if (check_desc(desc, false) != WISP_OK) return 0;
+size_t wisp_accept_workspace_size(const wisp_batch_desc *desc, int32_t vocab) {
+  if (check_desc(desc, false) != WISP_OK || vocab <= 0) return 0;
   Plan p;
-  make_plan(p, nullptr, desc, false);
+  make_plan(p, nullptr, desc, false, vocab);
   return p.total;
 }
 
@@ -426,9 +530,11 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
   else
     st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
   if (st != WISP_OK) return st;
-  sampler(sd, p.B, p.M, p.V, target_logits, tokens, draft_probs, desc->temperature, rng_seed,
-          reinterpret_cast<float *>(ws + p.w_m), reinterpret_cast<float *>(ws + p.w_s),
-          reinterpret_cast<int32_t *>(ws + p.w_amax), accept_len, out_tokens, s);
+  {
+    ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.M * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
+    sampler(sd, p.B, p.M, p.V, target_logits, tokens, draft_probs, desc->temperature, rng_seed,
+            sampler_scratch(p, ws), accept_len, out_tokens, s);
+  }
   return hip_check("sampler launch");
 }
 
@@ -443,7 +549,7 @@ wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float 
   if (!logits || !tokens || !accept_len || !out_tokens || !workspace)
     return fail(WISP_E_INVALID, "NULL logits / tokens / outputs / workspace");
   Plan p;
-  make_plan(p, nullptr, desc, false);
+  make_plan(p, nullptr, desc, false, vocab);
   if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
   if (workspace_bytes < p.total)
     return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
@@ -453,8 +559,7 @@ wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float 
   StepDesc sd = step_desc(p, ws, desc, 0);
   clear_ints(sd.err, 1, s);
   sampler(sd, p.B, p.M, vocab, logits, tokens, draft_probs, desc->temperature, rng_seed,
-          reinterpret_cast<float *>(ws + p.w_m), reinterpret_cast<float *>(ws + p.w_s),
-          reinterpret_cast<int32_t *>(ws + p.w_amax), accept_len, out_tokens, s);
+          sampler_scratch(p, ws), accept_len, out_tokens, s);
   return hip_check("sampler launch");
 }
 
@@ -497,6 +602,31 @@ wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint3
   if (!out && n) return fail(WISP_E_INVALID, "out is NULL");
   uniform_draws(rng_seed, req_id, tag, row, n, out, (hipStream_t)stream);
   return hip_check("uniform launch");
+}
+
+wisp_status wisp_profile_enable(int on) {
+  if (!on) prof_collect();
+  g_prof.on = on != 0;
+  return WISP_OK;
+}
+
+wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops) {
+  if (kind < 0 || kind >= WISP_PROF_KINDS) return fail(WISP_E_INVALID, "profile kind %d", kind);
+  prof_collect();
+  if (ms) *ms = g_prof.ms[kind];
+  if (launches) *launches = g_prof.launches[kind];
+  if (bytes) *bytes = g_prof.bytes[kind];
+  if (flops) *flops = g_prof.flops[kind];
+  return WISP_OK;
+}
+
+wisp_status wisp_profile_reset(void) {
+  prof_collect();
+  for (int k = 0; k < WISP_PROF_KINDS; ++k) {
+    g_prof.ms[k] = g_prof.bytes[k] = g_prof.flops[k] = 0.0;
+    g_prof.launches[k] = 0;
+  }
+  return WISP_OK;
 }
 
 wisp_status wisp_check(void *workspace, void *stream) {

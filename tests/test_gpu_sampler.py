@@ -54,8 +54,8 @@ def _batch(B, V, gmax, seed, T_draft=1.0, sigma=0.7, scale=1.3, gmin=0):
 def _gpu_accept(gamma, logits, toks, q, T, seed, req_id=None):
     B = gamma.shape[0]
     desc = W.BatchDesc(np.zeros(B, np.int32), gamma, None, T, req_id)
-    ws = W.workspace(W.wisp_accept_workspace_size(desc))
     V = logits.shape[1]
+    ws = W.workspace(W.wisp_accept_workspace_size(desc, V))
     dl = torch.from_numpy(logits).cuda()
     dt = torch.from_numpy(toks).cuda()
     dq = torch.from_numpy(q).cuda() if q.shape[0] else torch.zeros(1, device="cuda")
@@ -114,7 +114,7 @@ def test_out_of_range_draft_token_is_reported():
     toks = np.array([0, V + 5, 1], np.int32)
     q = np.full((2, V), 1.0 / V, np.float32)
     desc = W.BatchDesc(np.zeros(1, np.int32), gamma, None, 1.0)
-    ws = W.workspace(W.wisp_accept_workspace_size(desc))
+    ws = W.workspace(W.wisp_accept_workspace_size(desc, V))
     acc = torch.zeros(1, dtype=torch.int32, device="cuda")
     out = torch.zeros(3, dtype=torch.int32, device="cuda")
     W.wisp_accept(desc, V, torch.from_numpy(logits).cuda(), torch.from_numpy(toks).cuda(),

@@ -17,6 +17,9 @@ distributions are described in the repository's design notes.
 """
 from __future__ import annotations
 
+import ctypes
+import os
+import subprocess
 import zlib
 from dataclasses import dataclass, field
 
@@ -96,6 +99,35 @@ def hashed_u32(key: tuple[int, int], start: int, n: int, device) -> torch.Tensor
     return h
 
 
+# host implementation of the same generator (C, OpenMP): bitwise the same values
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_GEN_SRC = os.path.join(_HERE, "gen.c")
+_GEN_LIB = os.path.join(_HERE, "libwisp_inputs.so")
+_gen = None
+
+
+def build_host_generator(force: bool = True) -> str:
+    if force or not os.path.exists(_GEN_LIB) or os.path.getmtime(_GEN_LIB) < os.path.getmtime(_GEN_SRC):
+        tmp = _GEN_LIB + ".tmp"
+        subprocess.check_call(["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _GEN_SRC])
+        os.replace(tmp, _GEN_LIB)
+    return _GEN_LIB
+
+
+def _host_gen():
+    global _gen
+    if _gen is None:
+        build_host_generator(force=False)
+        L = ctypes.CDLL(_GEN_LIB)
+        vp, u32, u64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
+        for f in ("gen_table16", "gen_table32"):
+            getattr(L, f).argtypes = [vp, u32, u32, u64, u64, vp]
+        for f in ("gen_kv16", "gen_kv32"):
+            getattr(L, f).argtypes = [u32, u32, u64, u64, vp]
+        _gen = L
+    return _gen
+
+
 _QTABLE: dict = {}
 
 
@@ -111,6 +143,7 @@ def _normal_table(std: float, dtype: torch.dtype) -> torch.Tensor:
 
 
 _CHUNK = 1 << 24
+_FORCE_TORCH_GEN = False   # tests flip this to compare the two implementations
 
 
 def normal_tensor(seed: int, name: str, shape, std: float, dtype: torch.dtype,
@@ -126,6 +159,11 @@ def normal_tensor(seed: int, name: str, shape, std: float, dtype: torch.dtype,
     flat = out.view(-1)
     assert flat.numel() == n
     key = _key32(seed, name)
+    if flat.device.type == "cpu" and not _FORCE_TORCH_GEN:
+        f = _host_gen().gen_table16 if dtype == torch.bfloat16 else _host_gen().gen_table32
+        assert dtype in (torch.bfloat16, torch.float32)
+        f(table.data_ptr(), key[0], key[1], 0, n, flat.data_ptr())
+        return out.view(*shape)
     for s in range(0, n, _CHUNK):
         m = min(_CHUNK, n - s)
         h = hashed_u32(key, s, m, device)
@@ -144,6 +182,14 @@ def kv_values(seed: int, layer: int, req: int, start_pos: int, n_pos: int, n_kv:
     """
     per_pos = 2 * n_kv * hd
     key = _key32(seed, "kv", layer, req)
+    if torch.device(device).type == "cpu" and not _FORCE_TORCH_GEN:
+        n = n_pos * per_pos
+        out = torch.empty(n, dtype=dtype)
+        f = _host_gen().gen_kv16 if dtype == torch.bfloat16 else _host_gen().gen_kv32
+        assert dtype in (torch.bfloat16, torch.float32)
+        f(key[0], key[1], start_pos * per_pos, n, out.data_ptr())
+        v = out.view(n_pos, 2, n_kv, hd)
+        return v[:, 0], v[:, 1]
     h = hashed_u32(key, start_pos * per_pos, n_pos * per_pos, device)
     k8 = (h >> 24).to(torch.float32)
     v = ((k8 * 2.0 - 255.0) * (1.0 / 128.0)).to(dtype).view(n_pos, 2, n_kv, hd)
