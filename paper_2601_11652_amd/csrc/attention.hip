@@ -3,7 +3,7 @@
 // kv head h attend to keys 0 .. ctx_len_i + j (row j), read page by page through the
 // request's block table.
 //
-// bf16 path, one wave per work item (request, kv head, group of <= 64 query rows, token
+// bf16 path, one wave per work item (request, kv head, group of <= 48 query rows, token
 // chunk).  Per 32 tokens (two pages) the wave computes S^T = K Q^T and O^T += V^T P^T with
 // v_mfma_f32_16x16x32_bf16.  Computing the transposed products keeps every query row in
 // one lane column (lane % 16), so the online softmax needs only two cross-lane steps, and
@@ -16,7 +16,7 @@
 
 namespace wisp {
 
-template <int HD>
+template <int HD, int RB>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnItem *__restrict__ items,
                                                         int n_items, const uint16_t *__restrict__ q,
                                                         const uint16_t *__restrict__ kp,
@@ -26,7 +26,6 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
                                                         float scale) {
   constexpr int KC = HD / 32;   // 32-wide chunks of the QK^T contraction
   constexpr int MB = HD / 16;   // 16-wide blocks of the output head dimension
-  constexpr int RB = 4;         // 16-row query blocks per item
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int it = blockIdx.x * 4 + wave;
   if (it >= n_items) return;
@@ -35,7 +34,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
   const int G = nq / nkv;
   const int gam = d.gamma[i], ctx = d.ctx[i], off = d.off[i];
   const int rows = (gam + 1) * G;
-  const int lr0 = rbg * 64;
+  const int lr0 = rbg * (16 * RB);
   const int nrb = min(RB, (rows - lr0 + 15) >> 4);
   const int lc = lane & 15, lg = lane >> 4;
 
@@ -43,17 +42,12 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
   int jrow[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int lr = lr0 + rb * 16 + lc;
+    const int lr = min(lr0 + rb * 16 + lc, rows - 1);   // padding rows reuse a real row
     jrow[rb] = lr / G;
+    const int head = kvh * G + lr % G;
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (rb < nrb && lr < rows) {
-        const int head = kvh * G + lr % G;
-        v = *reinterpret_cast<const uint4 *>(q + ((int64_t)(off + jrow[rb]) * nq + head) * HD + kc * 32 + 8 * lg);
-      }
-      qf[rb][kc] = as_bf16x8(v);
-    }
+    for (int kc = 0; kc < KC; ++kc)
+      qf[rb][kc] = as_bf16x8(ld16(q + ((int64_t)(off + jrow[rb]) * nq + head) * HD + kc * 32 + 8 * lg));
   }
 
   float m_run[RB], l_run[RB];
@@ -68,36 +62,45 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
 
   const int32_t *pt = d.page_table + (int64_t)i * d.pt_stride;
   const int page_elems = kPage * HD;
-  for (int tp = item.t0; tp < item.t1; tp += 32) {
+  // Block ids of up to 64 pages live in one register (lane l holds page base + l) and are
+  // picked with readlane, so a K/V load never waits on a page-table load.
+  const int n_pages = (item.t1 + 15) >> 4;
+  int pbase = item.t0 >> 4;
+  int bids = pt[min(pbase + lane, n_pages - 1)];
+  auto block_of = [&](int pg) {
+    if (pg >= pbase + 64) {   // wave-uniform: move the window
+      pbase = pg;
+      bids = pt[min(pbase + lane, n_pages - 1)];
+    }
+    return __builtin_amdgcn_readlane(bids, pg - pbase);
+  };
+  // K and V of the page pair starting at token tp.  Block ids are clamped into the pool:
+  // tokens past the chunk end get zero probability, and an invalid id is reported.
+  auto load_pair = [&](int tp, bf16x8_t (&kf)[2][KC], bf16x8_t (&vf)[MB]) {
     const int pg = tp >> 4;
     const bool has1 = tp + 16 < item.t1;
-    int b0 = pt[pg];
-    int b1 = has1 ? pt[pg + 1] : 0;
-    bool ok0 = b0 >= 0 && b0 < d.n_blocks;
-    bool ok1 = has1 && b1 >= 0 && b1 < d.n_blocks;
-    if ((!ok0 || (has1 && !ok1)) && lane == 0) flag_error(d.err, kErrBlock);
+    int b0 = block_of(pg);
+    int b1 = has1 ? block_of(pg + 1) : b0;
+    if ((b0 < 0 || b0 >= d.n_blocks || b1 < 0 || b1 >= d.n_blocks) && lane == 0) flag_error(d.err, kErrBlock);
+    b0 = min(max(b0, 0), d.n_blocks - 1);
+    b1 = min(max(b1, 0), d.n_blocks - 1);
     const uint16_t *K0 = kp + ((int64_t)b0 * nkv + kvh) * page_elems;
     const uint16_t *K1 = kp + ((int64_t)b1 * nkv + kvh) * page_elems;
     const uint16_t *V0 = vp + ((int64_t)b0 * nkv + kvh) * page_elems;
     const uint16_t *V1 = vp + ((int64_t)b1 * nkv + kvh) * page_elems;
-    bf16x8_t kf[2][KC];
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
-      uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-      if (ok0) a = *reinterpret_cast<const uint4 *>(K0 + kc * 512 + lane * 8);
-      if (ok1) b = *reinterpret_cast<const uint4 *>(K1 + kc * 512 + lane * 8);
-      kf[0][kc] = as_bf16x8(a);
-      kf[1][kc] = as_bf16x8(b);
+      kf[0][kc] = as_bf16x8(ld16(K0 + kc * 512 + lane * 8));
+      kf[1][kc] = as_bf16x8(ld16(K1 + kc * 512 + lane * 8));
     }
-    bf16x8_t vf[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
-      uint2 a = make_uint2(0, 0), b = make_uint2(0, 0);
-      if (ok0) a = *reinterpret_cast<const uint2 *>(V0 + mb * 256 + lane * 4);
-      if (ok1) b = *reinterpret_cast<const uint2 *>(V1 + mb * 256 + lane * 4);
+      const uint2 a = *reinterpret_cast<const uint2 *>(V0 + mb * 256 + lane * 4);
+      const uint2 b = *reinterpret_cast<const uint2 *>(V1 + mb * 256 + lane * 4);
       vf[mb] = as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
     }
-
+  };
+  auto compute_pair = [&](int tp, const bf16x8_t (&kf)[2][KC], const bf16x8_t (&vf)[MB]) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       if (rb >= nrb) break;
@@ -149,9 +152,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
         o[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[mb], pb, o[rb][mb], 0, 0, 0);
       }
     }
+  };
+
+  // two register sets: the next page pair loads while the current one computes
+  bf16x8_t kA[2][KC], vA[MB], kB[2][KC], vB[MB];
+  load_pair(item.t0, kA, vA);
+  for (int tp = item.t0; tp < item.t1; tp += 64) {
+    const bool has2 = tp + 32 < item.t1;
+    if (has2) load_pair(tp + 32, kB, vB);
+    compute_pair(tp, kA, vA);
+    if (!has2) break;
+    if (tp + 64 < item.t1) load_pair(tp + 64, kA, vA);
+    compute_pair(tp + 32, kB, vB);
   }
 
-  // partials: O [item][hd][64 rows] (unnormalised), (m, l) [item][64 rows]
+  // partials: O [item][hd][64 row slots] (unnormalised), (m, l) [item][64 row slots]
   float *po = part_o + (int64_t)it * HD * 64;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -179,12 +194,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
   const AttnGroup g = groups[blockIdx.x];
   const int G = nq / nkv;
   const int rows = (d.gamma[g.req] + 1) * G;
-  const int lr0 = g.rbg * 64;
-  const int nr = min(64, rows - lr0);
+  const int lr0 = g.rbg * kAttnRowsPerItem;
+  const int nr = min(kAttnRowsPerItem, rows - lr0);
   const int off = d.off[g.req];
   constexpr int CH = HD / 8;
   for (int u = threadIdx.x; u < nr * CH; u += 256) {
-    const int rr = u / CH, c0 = (u % CH) * 8;
+    const int rr = u % nr, c0 = (u / nr) * 8;   // neighbouring lanes read neighbouring rows
     float m = -INFINITY;
     for (int c = 0; c < g.n_items; ++c) m = fmaxf(m, part_ml[((int64_t)(g.first_item + c) * 64 + rr) * 2]);
     float den = 0.f;
@@ -221,11 +236,12 @@ void attention_bf16(const StepDesc &d, const AttnItem *items, int n_items, const
   if (n_items == 0) return;
   const float scale = 1.0f / sqrtf((float)hd);
   const int blocks = (n_items + 3) / 4;
+  constexpr int RB = kAttnRowsPerItem / 16;
   if (hd == 128) {
-    attn_bf16_kernel<128><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
+    attn_bf16_kernel<128, RB><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
     attn_combine_kernel<128><<<n_groups, 256, 0, s>>>(d, groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
   } else {
-    attn_bf16_kernel<64><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
+    attn_bf16_kernel<64, RB><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
     attn_combine_kernel<64><<<n_groups, 256, 0, s>>>(d, groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
   }
 }

@@ -58,7 +58,7 @@ struct AttnItem {   // one wave's work: request, kv head, row group, token range
 struct AttnGroup {  // the chunks of one (request, kv head, row group), combined in order
   int32_t req, kvh, rbg, first_item, n_items, pad0, pad1, pad2;
 };
-constexpr int kAttnRowsPerItem = 64;   // query rows one wave carries (4 blocks of 16)
+constexpr int kAttnRowsPerItem = 48;   // query rows one wave carries (3 blocks of 16)
 
 void attention_bf16(const StepDesc &d, const AttnItem *items, int n_items, const AttnGroup *groups,
                     int n_groups, const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
