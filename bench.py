@@ -28,6 +28,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# timing classes of the library's profiling hook (include/wisp.h) and the kernels they cover
+KERNEL_CLASSES = ((0, "gemm_ring1"), (1, "gemm_ring2"), (2, "gemm_tiled"), (3, "attention"),
+                  (4, "attention_combine"), (5, "rows"), (6, "sampler"))
+KERNEL_NAMES = {"gemm_ring1": "gemm_ring_kernel<1, 4, MT, 1, 8>", "gemm_ring2": "gemm_ring_kernel<1, 4, MT, 2, 4>",
+                "gemm_tiled": "gemm_bf16_kernel", "attention": "attn_bf16_kernel",
+                "attention_combine": "attn_combine_kernel", "rows": "row kernels", "sampler": "sampler kernels"}
 BF16_PEAK_TFLOPS = 2516.6
 FP32_PEAK_TFLOPS = 157.3
 
@@ -222,7 +228,7 @@ def main():
     torch.cuda.synchronize()
     classes = {}
     import ctypes as C
-    for kind, name in ((0, "gemm"), (1, "attention"), (2, "rows"), (3, "sampler")):
+    for kind, name in KERNEL_CLASSES:
         ms, n, by, fl = C.c_double(), C.c_int64(), C.c_double(), C.c_double()
         W.lib.wisp_profile_read(kind, C.byref(ms), C.byref(n), C.byref(by), C.byref(fl))
         if n.value:
@@ -232,15 +238,15 @@ def main():
                              "achieved_GBs": by.value / ms.value / 1e6 if ms.value else 0.0,
                              "achieved_TFLOPs": fl.value / ms.value / 1e9 if ms.value else 0.0}
     W.lib.wisp_profile_enable(0)
-    dom = max(("gemm", "attention"), key=lambda k: classes.get(k, {}).get("ms_per_step", 0.0))
+    dom = max((k for k in classes if classes[k]["bytes_per_launch"] > 0), key=lambda k: classes[k]["ms_per_step"])
     c = classes[dom]
-    mfma_bound = dom == "gemm" and M >= 630
+    mfma_bound = dom.startswith("gemm") and M >= 630
     if mfma_bound:
         roof = {"bound": "mfma", "achieved": c["achieved_TFLOPs"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
     else:
         roof = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["kernel"] = "dense projections (gemm_ring_kernel / gemm_bf16_kernel)" if dom == "gemm" else "attn_bf16_kernel + attn_combine_kernel"
+    roof["kernel"] = KERNEL_NAMES[dom]
     tr = traffic_from_counters(f"{dom}_{args.config}")
     roof["traffic"] = tr
 

@@ -187,20 +187,24 @@ wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint3
 wisp_status wisp_check(void *workspace, void *stream);
 
 /*
- * Opt-in timing of wisp_verify's kernels by class (instrumentation for benchmarks; off by
+ * Opt-in timing of wisp_verify's kernels by kernel (instrumentation for benchmarks; off by
  * default, process-wide, not thread-safe).  While enabled, each launch of a class is
  * bracketed by HIP events on the caller's stream, and the class accumulates the measured
- * milliseconds, the launch count and the algorithmic bytes / flops of its launches
- *   GEMM: 2-byte (bf16) or 4-byte weights N*K + activations M*K, fp32 result M*N;
+ * milliseconds, the launch count and the algorithmic bytes / flops of its launches:
+ *   GEMM classes: 2-byte (bf16) or 4-byte weights N*K + activations M*K + fp32 result M*N;
  *   ATTN: K and V bytes of every token each kv head reads (ctx_len + gamma + 1 per request);
- *   SAMPLER: two passes over the fp32 logits plus one row per request.
+ *   SAMPLER: two passes over the fp32 logits plus one row per request;
+ *   ATTN_COMBINE, ROWS: none (overhead kernels).
  * wisp_profile_read synchronises on the recorded events.
  */
-#define WISP_PROF_GEMM 0
-#define WISP_PROF_ATTN 1
-#define WISP_PROF_ROWS 2
-#define WISP_PROF_SAMPLER 3
-#define WISP_PROF_KINDS 4
+#define WISP_PROF_GEMM_RING1 0   /* gemm_ring_kernel, one 32-column fragment per wave   */
+#define WISP_PROF_GEMM_RING2 1   /* gemm_ring_kernel, two 32-column fragments per wave  */
+#define WISP_PROF_GEMM_TILED 2   /* gemm_bf16_kernel (large M) and the fp32 GEMM         */
+#define WISP_PROF_ATTN 3         /* attn_bf16_kernel / attn_f32_kernel                   */
+#define WISP_PROF_ATTN_COMBINE 4 /* attn_combine_kernel                                  */
+#define WISP_PROF_ROWS 5         /* embedding, norms, RoPE + KV append, SwiGLU           */
+#define WISP_PROF_SAMPLER 6      /* acceptance kernels                                    */
+#define WISP_PROF_KINDS 7
 wisp_status wisp_profile_enable(int on);
 wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops);
 wisp_status wisp_profile_reset(void);

@@ -229,21 +229,27 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
   }
 }
 
-void attention_bf16(const StepDesc &d, const AttnItem *items, int n_items, const AttnGroup *groups,
-                    int n_groups, const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
-                    float *part_o, float *part_ml, uint16_t *out, bool out_packed, int out_K, int nq,
-                    int nkv, int hd, hipStream_t s) {
+void attention_bf16_main(const StepDesc &d, const AttnItem *items, int n_items, const uint16_t *q,
+                         const uint16_t *k_pool, const uint16_t *v_pool, float *part_o, float *part_ml,
+                         int nq, int nkv, int hd, hipStream_t s) {
   if (n_items == 0) return;
   const float scale = 1.0f / sqrtf((float)hd);
   const int blocks = (n_items + 3) / 4;
   constexpr int RB = kAttnRowsPerItem / 16;
-  if (hd == 128) {
+  if (hd == 128)
     attn_bf16_kernel<128, RB><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
-    attn_combine_kernel<128><<<n_groups, 256, 0, s>>>(d, groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
-  } else {
+  else
     attn_bf16_kernel<64, RB><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
+}
+
+void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_groups,
+                            const float *part_o, const float *part_ml, uint16_t *out, bool out_packed,
+                            int out_K, int nq, int nkv, int hd, hipStream_t s) {
+  if (n_groups == 0) return;
+  if (hd == 128)
+    attn_combine_kernel<128><<<n_groups, 256, 0, s>>>(d, groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
+  else
     attn_combine_kernel<64><<<n_groups, 256, 0, s>>>(d, groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
-  }
 }
 
 // ---------------------------------------------------------------------------------------

@@ -60,10 +60,13 @@ struct AttnGroup {  // the chunks of one (request, kv head, row group), combined
 };
 constexpr int kAttnRowsPerItem = 48;   // query rows one wave carries (3 blocks of 16)
 
-void attention_bf16(const StepDesc &d, const AttnItem *items, int n_items, const AttnGroup *groups,
-                    int n_groups, const uint16_t *q, const uint16_t *k_pool, const uint16_t *v_pool,
-                    float *part_o, float *part_ml, uint16_t *out, bool out_packed, int out_K, int nq,
-                    int nkv, int hd, hipStream_t s);
+// split-KV partials of every item, then their fixed-order combine into `out`
+void attention_bf16_main(const StepDesc &d, const AttnItem *items, int n_items, const uint16_t *q,
+                         const uint16_t *k_pool, const uint16_t *v_pool, float *part_o, float *part_ml,
+                         int nq, int nkv, int hd, hipStream_t s);
+void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_groups,
+                            const float *part_o, const float *part_ml, uint16_t *out, bool out_packed,
+                            int out_K, int nq, int nkv, int hd, hipStream_t s);
 void attention_f32(const StepDesc &d, int B, const float *q, const float *k_pool,
                    const float *v_pool, float *out, int nq, int nkv, int hd, int max_tokens,
                    hipStream_t s);

@@ -366,6 +366,11 @@ StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_bloc
   return sd;
 }
 
+int gemm_class(const Plan &p, const GemmCfg &c) {
+  if (!p.bf16 || c.kind == 0) return WISP_PROF_GEMM_TILED;
+  return c.kind == 1 ? WISP_PROF_GEMM_RING1 : WISP_PROF_GEMM_RING2;
+}
+
 wisp_status hip_check(const char *what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(WISP_E_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -411,7 +416,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
     T *vl = (T *)kv->v_pool + l * layer_elems;
     // one dense projection: C = act . W^T (fp32 partials over cfg.splits K ranges)
     auto gemm = [&](const T *act, const void *w, float *out, int N, int K, const GemmCfg &cfg) {
-      ProfScope ps(WISP_PROF_GEMM, gemm_bytes(N, K), gemm_flops(N, K), s);
+      ProfScope ps(gemm_class(p, cfg), gemm_bytes(N, K), gemm_flops(N, K), s);
       if (p.bf16)
         gemm_bf16((const uint16_t *)act, (const uint16_t *)w, out, p.M, N, K, N, cfg, s);
       else
@@ -423,16 +428,21 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
       ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
       qkv_rope_append<T>(sd, part, sq, cs, qb, kl, vl, p.M, p.nq, p.nkv, p.hd, s);
     }
-    {
+    if (p.bf16) {
+      float *po = reinterpret_cast<float *>(ws + p.w_attn_o);
+      float *pml = reinterpret_cast<float *>(ws + p.w_attn_ml);
+      {
+        ProfScope ps(WISP_PROF_ATTN, attn_bytes, attn_flops, s);
+        attention_bf16_main(sd, items, (int)p.items.size(), (const uint16_t *)qb, (const uint16_t *)kl,
+                            (const uint16_t *)vl, po, pml, p.nq, p.nkv, p.hd, s);
+      }
+      ProfScope ps(WISP_PROF_ATTN_COMBINE, 0, 0, s);
+      attention_bf16_combine(sd, groups, (int)p.groups.size(), po, pml, (uint16_t *)ao, true, p.qdim, p.nq,
+                             p.nkv, p.hd, s);
+    } else {
       ProfScope ps(WISP_PROF_ATTN, attn_bytes, attn_flops, s);
-      if (p.bf16)
-        attention_bf16(sd, items, (int)p.items.size(), groups, (int)p.groups.size(), (const uint16_t *)qb,
-                       (const uint16_t *)kl, (const uint16_t *)vl, reinterpret_cast<float *>(ws + p.w_attn_o),
-                       reinterpret_cast<float *>(ws + p.w_attn_ml), (uint16_t *)ao, true, p.qdim, p.nq,
-                       p.nkv, p.hd, s);
-      else
-        attention_f32(sd, p.B, (const float *)qb, (const float *)kl, (const float *)vl, (float *)ao, p.nq,
-                      p.nkv, p.hd, p.max_tokens, s);
+      attention_f32(sd, p.B, (const float *)qb, (const float *)kl, (const float *)vl, (float *)ao, p.nq,
+                    p.nkv, p.hd, p.max_tokens, s);
     }
     const int so = gemm(ao, m->w_o[l], part, p.d, p.qdim, p.g_o);
     {
@@ -452,7 +462,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
     }
   }
   {
-    ProfScope ps(WISP_PROF_GEMM, gemm_bytes(p.V, p.d), gemm_flops(p.V, p.d), s);
+    ProfScope ps(gemm_class(p, p.g_lm), gemm_bytes(p.V, p.d), gemm_flops(p.V, p.d), s);
     if (p.bf16)
       gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.M, p.V, p.d, p.V, p.g_lm, s);
     else
@@ -586,10 +596,12 @@ wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wis
   if (p.bf16) {
     const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
     const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
-    attention_bf16(sd, items, (int)p.items.size(), groups, (int)p.groups.size(), (const uint16_t *)q,
-                   (const uint16_t *)kv->k_pool, (const uint16_t *)kv->v_pool,
-                   reinterpret_cast<float *>(ws + p.w_attn_o), reinterpret_cast<float *>(ws + p.w_attn_ml),
-                   (uint16_t *)out, false, p.qdim, p.nq, p.nkv, p.hd, s);
+    float *po = reinterpret_cast<float *>(ws + p.w_attn_o);
+    float *pml = reinterpret_cast<float *>(ws + p.w_attn_ml);
+    attention_bf16_main(sd, items, (int)p.items.size(), (const uint16_t *)q, (const uint16_t *)kv->k_pool,
+                        (const uint16_t *)kv->v_pool, po, pml, p.nq, p.nkv, p.hd, s);
+    attention_bf16_combine(sd, groups, (int)p.groups.size(), po, pml, (uint16_t *)out, false, p.qdim, p.nq,
+                           p.nkv, p.hd, s);
   } else {
     attention_f32(sd, p.B, (const float *)q, (const float *)kv->k_pool, (const float *)kv->v_pool,
                   (float *)out, p.nq, p.nkv, p.hd, p.max_tokens, s);

@@ -1,0 +1,97 @@
+"""The C ABI on the CPU: every function declared in include/wisp.h is exported by
+libwisp.so, and host-side validation returns the documented status before any launch."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wisp.h")
+
+
+@pytest.fixture(scope="module")
+def W():
+    import paper_2601_11652_amd as W
+    if not os.path.exists(W.LIB_PATH):
+        from paper_2601_11652_amd import build
+        build.build()
+    W.load_library()
+    return W
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(wisp_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_every_declared_symbol_is_exported(W):
+    names = _declared()
+    assert "wisp_verify" in names and "wisp_accept" in names and len(names) >= 10
+    for n in names:
+        assert hasattr(W.load_library(), n), n
+    assert set(W.EXPORTS) == set(names)
+
+
+FAKE = 0x1000  # never dereferenced: validation fails first
+
+
+def _model(W, **kw):
+    m = W.wisp_model(2, 256, 4, 4, 64, 1024, 1024, 1e-5, 1e4, W.WISP_F32, FAKE, FAKE, FAKE)
+    arr = (C.c_void_p * 2)(FAKE, FAKE)
+    for f in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down"):
+        setattr(m, f, C.cast(arr, C.POINTER(C.c_void_p)))
+    m._keep = arr
+    for k, v in kw.items():
+        setattr(m, k, v)
+    return m
+
+
+def _desc(W, ctx, gamma, stride=16, T=1.0):
+    d = W.BatchDesc(ctx, gamma, None, T)
+    d.c.kv_page_table = FAKE
+    d.c.pt_stride = stride
+    return d
+
+
+def _verify(W, model, desc, ws_bytes=1 << 40, kv_pages=16, tokens=FAKE):
+    L = W.load_library()
+    kv = W.wisp_kv(FAKE, FAKE, 100, kv_pages)
+    return L.wisp_verify(C.byref(model), C.byref(kv), C.byref(desc.c), tokens, FAKE, 1, FAKE, FAKE, FAKE,
+                         FAKE, ws_bytes, None)
+
+
+def test_validation_statuses(W):
+    m = _model(W)
+    assert _verify(W, m, _desc(W, [10], [17])) == W.WISP_E_INVALID
+    assert "gamma" in W.wisp_last_error()
+    assert _verify(W, m, _desc(W, [-1], [2])) == W.WISP_E_INVALID
+    assert _verify(W, m, _desc(W, [10], [2], T=-1.0)) == W.WISP_E_INVALID
+    assert _verify(W, m, _desc(W, [250], [8], stride=16)) == W.WISP_E_CAPACITY     # 259 > 256
+    assert _verify(W, m, _desc(W, [10], [2]), ws_bytes=64) == W.WISP_E_WORKSPACE
+    assert _verify(W, m, _desc(W, [10], [2]), kv_pages=8) == W.WISP_E_UNSUPPORTED
+    assert _verify(W, m, _desc(W, [10], [2]), tokens=None) == W.WISP_E_INVALID
+    assert _verify(W, _model(W, head_dim=48), _desc(W, [10], [2])) == W.WISP_E_UNSUPPORTED
+    assert _verify(W, _model(W, n_kv_heads=3), _desc(W, [10], [2])) == W.WISP_E_UNSUPPORTED
+    assert _verify(W, _model(W, dtype=W.WISP_BF16, head_dim=96, n_q_heads=4), _desc(W, [10], [2])) == W.WISP_E_UNSUPPORTED
+    assert _verify(W, _model(W, embed=None), _desc(W, [10], [2])) == W.WISP_E_INVALID
+    L = W.load_library()
+    assert L.wisp_verify(None, None, None, None, None, 0, None, None, None, None, 0, None) == W.WISP_E_INVALID
+    assert _verify(W, m, _desc(W, [], [])) == W.WISP_OK          # empty batch: nothing to do
+
+
+def test_workspace_size_and_pack_validation(W):
+    m = _model(W)
+    assert W.wisp_workspace_size(m, _desc(W, [10], [2])) > 0
+    assert W.wisp_workspace_size(m, _desc(W, [10], [17])) == 0
+    small = W.wisp_workspace_size(m, _desc(W, [10], [2]))
+    big = W.wisp_workspace_size(m, _desc(W, [10, 100, 7], [2, 16, 0]))
+    assert big > small
+    assert W.wisp_accept_workspace_size(_desc(W, [0], [3]), 0) == 0
+    L = W.load_library()
+    assert L.wisp_pack_linear(FAKE, FAKE, 30, 64, W.WISP_BF16, None) == W.WISP_E_UNSUPPORTED
+    assert L.wisp_pack_linear(FAKE, FAKE, 32, 8, W.WISP_BF16, None) == W.WISP_E_UNSUPPORTED
+    assert L.wisp_pack_linear(None, FAKE, 32, 16, W.WISP_BF16, None) == W.WISP_E_INVALID
+    assert L.wisp_pack_linear(FAKE, FAKE, 32, 16, 7, None) == W.WISP_E_UNSUPPORTED
