@@ -42,29 +42,6 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def fill_kv_device(kv, mix, pt_np):
-    """Synthetic cached context of every request, generated on the device and placed
-    through the page table in the documented page layout."""
-    import torch
-    import wisp_inputs as wi
-    s = mix.shape
-    dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
-    kidx = torch.as_tensor(wi.k_page_index(s.head_dim), device="cuda")
-    vidx = torch.as_tensor(wi.v_page_index(s.head_dim), device="cuda")
-    heads = torch.arange(s.n_kv_heads, device="cuda")[None, :, None]
-    for i in range(mix.B):
-        n = int(mix.ctx_len[i])
-        if n == 0:
-            continue
-        t = torch.arange(n, device="cuda")
-        blk = torch.as_tensor(pt_np[i], device="cuda")[t // 16][:, None, None]
-        slot = t % 16
-        for l in range(s.n_layers):
-            K, V = wi.kv_values(mix.seed, l, i, 0, n, s.n_kv_heads, s.head_dim, "cuda", dt)
-            kv.k[l][blk, heads, kidx[slot][:, None, :]] = K
-            kv.v[l][blk, heads, vidx[slot][:, None, :]] = V
-
-
 def gpu_draft_fixture(W, gm, kv, mix, pt, roots):
     """Draft tokens and q rows for the timed batch: q_j = softmax(l_{j-1} / T_i + sigma_i eps)
     from the target's own row j-1 (gamma = 0 verification calls), y_j ~ q_j."""
@@ -181,7 +158,7 @@ def main():
     dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
     kv = W.KVPool.zeros(s.n_layers, n_blocks, s.n_kv_heads, s.head_dim, dt)
     t0 = time.time()
-    fill_kv_device(kv, mix, pt_np)
+    wi.fill_kv_pool(kv.k, kv.v, mix, pt_np)
     torch.cuda.synchronize()
     log(f"KV pool {kv.k.numel() * 2 * kv.k.element_size() / 2**30:.2f} GiB filled in {time.time() - t0:.1f} s")
     pt = torch.as_tensor(pt_np, device="cuda")

@@ -264,8 +264,11 @@ class OracleModel:
             return C.cast(v, C.POINTER(C.c_void_p))
 
         s = shape
+        # the embedding table stays reachable so tests can perturb single entries
+        self.embed = _np_storage(glob["embed"])
+        self._keep.append(self.embed)
         self.s = _OrcModel(L, s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.d_ff, s.vocab,
-                           int(self.bf16), s.rms_eps, s.rope_base, arr(glob["embed"]),
+                           int(self.bf16), s.rms_eps, s.rope_base, self.embed.ctypes.data_as(C.c_void_p),
                            arr(glob["lm_head"]), arr(glob["final_norm"]), vec("attn_norm"),
                            vec("wq"), vec("wk"), vec("wv"), vec("wo"), vec("mlp_norm"),
                            vec("w_gate"), vec("w_up"), vec("w_down"))

@@ -44,23 +44,31 @@ def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=Non
     dt = torch.float32 if s.dtype == "f32" else torch.bfloat16
     reqs = range(mix.B) if requests is None else requests
     lays = range(s.n_layers) if layers is None else layers
+    hd = s.head_dim
+    kidx = wi.k_page_index(hd)
+    vidx = wi.v_page_index(hd)
     for i in reqs:
         n = int(mix.ctx_len[i])
         if n == 0:
             continue
+        key = i if req_keys is None else int(req_keys[i])
+        nf = n // wi.PAGE                     # full pages
+        full = page_table[i, :nf]
         for li, l in enumerate(lays):
-            key = i if req_keys is None else int(req_keys[i])
-            K, V = wi.kv_values(mix.seed, l, key, 0, n, s.n_kv_heads, s.head_dim, "cpu", dt)
+            K, V = wi.kv_values(mix.seed, l, key, 0, n, s.n_kv_heads, hd, "cpu", dt)
             Kn = _to_storage(K, s)
             Vn = _to_storage(V, s)
-            kidx = wi.k_page_index(s.head_dim)
-            vidx = wi.v_page_index(s.head_dim)
-            for t0 in range(0, n, wi.PAGE):
-                t1 = min(n, t0 + wi.PAGE)
-                blk = page_table[i, t0 // wi.PAGE]
-                sl = np.arange(t1 - t0)
-                kp[li, blk][:, kidx[sl]] = Kn[t0:t1].transpose(1, 0, 2)
-                vp[li, blk][:, vidx[sl]] = Vn[t0:t1].transpose(1, 0, 2)
+            if nf:
+                # K page: [dim/32][(dim%32)/8][slot][dim%8]; V page: [dim/16][slot/4][dim%16][slot%4]
+                k = Kn[:nf * wi.PAGE].reshape(nf, wi.PAGE, s.n_kv_heads, hd // 32, 4, 8)
+                kp[li, full] = k.transpose(0, 2, 3, 4, 1, 5).reshape(nf, s.n_kv_heads, -1)
+                v = Vn[:nf * wi.PAGE].reshape(nf, 4, 4, s.n_kv_heads, hd // 16, 16)
+                vp[li, full] = v.transpose(0, 3, 4, 1, 5, 2).reshape(nf, s.n_kv_heads, -1)
+            if n > nf * wi.PAGE:
+                blk = page_table[i, nf]
+                sl = np.arange(n - nf * wi.PAGE)
+                kp[li, blk][:, kidx[sl]] = Kn[nf * wi.PAGE:].transpose(1, 0, 2)
+                vp[li, blk][:, vidx[sl]] = Vn[nf * wi.PAGE:].transpose(1, 0, 2)
 
 
 def prefill_context(model: OracleModel, mix: wi.Mix, pools, page_table, requests=None):
@@ -102,6 +110,30 @@ def draft_fixture(model: OracleModel, mix: wi.Mix, pools, page_table, roots, req
     return ({i: np.array(toks[i], np.int32) for i in reqs},
             {i: (np.stack(qs[i]) if qs[i] else np.zeros((0, V), np.float32)) for i in reqs},
             {i: (np.stack(lgs[i]) if lgs[i] else np.zeros((0, V), np.float32)) for i in reqs})
+
+
+class perturbed_embedding:
+    """Context manager: moves embedding entries (token, col) of a host model by one unit in
+    the last place of their storage format, and restores them on exit.  Used to measure how
+    far the model's own rounding noise carries a minimal input change."""
+
+    def __init__(self, model: OracleModel, token: int, cols=(17, 2011)):
+        self.e = model.embed
+        self.token = int(token)
+        self.cols = [c % self.e.shape[1] for c in cols]
+        self.saved = None
+
+    def __enter__(self):
+        self.saved = self.e[self.token, self.cols].copy()
+        if self.e.dtype == np.uint16:
+            self.e[self.token, self.cols] = self.saved + 1          # next bf16 bit pattern
+        else:
+            self.e[self.token, self.cols] = np.nextafter(self.saved, np.float32(np.inf))
+        return self
+
+    def __exit__(self, *exc):
+        self.e[self.token, self.cols] = self.saved
+        return False
 
 
 def random_drafts(mix: wi.Mix, requests, roots, tag: int = 9):

@@ -94,12 +94,16 @@ def rel_row_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
 
 
 def compare_decisions(acc_gpu, out_gpu, ref: oracle.AcceptResult, gamma, tokens, u_margin: float,
-                      key_margin: float, residual_exempt: bool = False):
+                      key_margin: float, residual_exempt: bool = False, logit_gap=0.0):
     """GPU decisions vs the oracle's on its own logits.  Returns (n_decisions, mismatches,
     unflagged) where a mismatch is unflagged if no draw of the oracle's path was within the
     margins (|u - a| < u_margin on an acceptance, or top-two race keys within key_margin).
     With residual_exempt, the extra token after a rejection is not compared (used when the
-    two sides' logits differ by more than rounding)."""
+    two sides' logits differ by more than rounding).  logit_gap (scalar or per request) is
+    the max-abs difference of the two sides' logits: p/q moves by at most a factor
+    exp(2 * gap), which widens the acceptance margin by that relative amount, and the race
+    margin by 4 * gap."""
+    gaps = np.broadcast_to(np.asarray(logit_gap, dtype=np.float64), (len(gamma),))
     off = np.concatenate([[0], np.cumsum(gamma + 1)])
     doff = np.concatenate([[0], np.cumsum(gamma)])
     n_dec = 0
@@ -116,9 +120,12 @@ def compare_decisions(acc_gpu, out_gpu, ref: oracle.AcceptResult, gamma, tokens,
         mism += 1
         u = ref.acc_u[doff[i]:doff[i] + nd]
         a = ref.acc_a[doff[i]:doff[i] + nd]
-        flag = bool(np.any(np.abs(u - a) < u_margin))
+        widen = np.expm1(2.0 * gaps[i])
+        flag = bool(np.any(np.abs(u - a) < u_margin + a * widen))
         k1, k2 = ref.race_key1[i], ref.race_key2[i]
-        if acc_gpu[i] == L and abs(k1 - k2) < key_margin * max(1.0, abs(k1)):
+        # race keys are score - ln(-ln u) with score a log-probability or scaled logit: a
+        # logit gap moves each key by at most 2 * gap, the difference of two by 4 * gap
+        if acc_gpu[i] == L and abs(k1 - k2) < key_margin * max(1.0, abs(k1)) + 4.0 * gaps[i]:
             flag = True
         if residual_exempt and acc_gpu[i] == L and L < gamma[i]:
             flag = True       # residual keys ln(p - q) are not Lipschitz in the logits

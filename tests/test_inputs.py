@@ -60,3 +60,35 @@ def test_workload_mixes():
     pt, nb = wi.page_table(wi.make_mix("8b_b32"))
     used = pt[pt >= 0]
     assert len(np.unique(used)) == len(used) and used.max() < nb
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_context_kv_placement_agrees_slot_by_slot(dtype):
+    """The oracle's host placement and the device-side fill put every context position's
+    K and V at the slot the page table and page layout name (checked one slot at a time),
+    and touch nothing else."""
+    import torch
+    from oracle import fixtures as fx
+    shape = wi.ModelShape("place", 2, 256, 4, 2, 64, 512, 1024, dtype, 1e4)
+    mix = wi.custom_mix(shape, [37, 16, 0, 50, 1], [1, 2, 0, 3, 16])
+    pt, nb = wi.page_table(mix)
+    host = fx.empty_pools(shape, nb)
+    fx.place_synthetic_kv(mix, host, pt)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    dev_k = torch.zeros(shape.n_layers, nb, shape.n_kv_heads, 16 * shape.head_dim, dtype=tdt)
+    dev_v = torch.zeros_like(dev_k)
+    wi.fill_kv_pool(dev_k, dev_v, mix, pt)
+    ref = fx.empty_pools(shape, nb)
+    kidx, vidx = wi.k_page_index(shape.head_dim), wi.v_page_index(shape.head_dim)
+    for i in range(mix.B):
+        n = int(mix.ctx_len[i])
+        for l in range(shape.n_layers):
+            K, V = wi.kv_values(mix.seed, l, i, 0, n, shape.n_kv_heads, shape.head_dim, "cpu", tdt)
+            K, V = fx._to_storage(K, shape), fx._to_storage(V, shape)
+            for t in range(n):
+                for h in range(shape.n_kv_heads):
+                    ref[0][l, pt[i, t // 16], h, kidx[t % 16]] = K[t, h]
+                    ref[1][l, pt[i, t // 16], h, vidx[t % 16]] = V[t, h]
+    for w, dev in ((0, dev_k), (1, dev_v)):
+        np.testing.assert_array_equal(host[w], ref[w])
+        np.testing.assert_array_equal(fx._to_storage(dev, shape), ref[w])

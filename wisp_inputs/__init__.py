@@ -234,6 +234,32 @@ def slots_from_pages(p, which: str, hd: int):
     return p[..., idx]
 
 
+def fill_kv_pool(k_pool: torch.Tensor, v_pool: torch.Tensor, mix: "Mix", page_table: np.ndarray,
+                 requests=None, req_keys=None):
+    """Place the synthetic cached context of the given requests (default: all) into pools
+    [n_layers][n_blocks][n_kv][16 * head_dim] on any device, through the page table.
+    req_keys[r] (default the request index) keys request r's generated values."""
+    s = mix.shape
+    dev = k_pool.device
+    dt = k_pool.dtype
+    kidx = torch.as_tensor(k_page_index(s.head_dim), device=dev)
+    vidx = torch.as_tensor(v_page_index(s.head_dim), device=dev)
+    heads = torch.arange(s.n_kv_heads, device=dev)[None, :, None]
+    reqs = range(mix.B) if requests is None else requests
+    for n_i, i in enumerate(reqs):
+        n = int(mix.ctx_len[i])
+        if n == 0:
+            continue
+        key = i if req_keys is None else int(req_keys[n_i])
+        t = torch.arange(n, device=dev)
+        blk = torch.as_tensor(page_table[n_i if requests is not None else i], device=dev)[t // PAGE][:, None, None]
+        slot = t % PAGE
+        for l in range(s.n_layers):
+            K, V = kv_values(mix.seed, l, key, 0, n, s.n_kv_heads, s.head_dim, dev, dt)
+            k_pool[l][blk, heads, kidx[slot][:, None, :]] = K
+            v_pool[l][blk, heads, vidx[slot][:, None, :]] = V
+
+
 # --------------------------------------------------------------------------------------
 # model weights (natural layout: every linear map is [out_features][in_features])
 # --------------------------------------------------------------------------------------
