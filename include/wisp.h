@@ -80,10 +80,11 @@ typedef struct {
  * table, Sec. 4.5).  Two DEVICE pools of `dtype`, each
  *   [n_layers][n_blocks][n_kv_heads][page of 16 * head_dim elements].
  * Inside one page (one block, one kv head) element (slot s, dim e) sits at
- *   K:  ((e / 32) * 4 + (e % 32) / 8) * 128 + s * 8 + e % 8
- *   V:  ((e / 16) * 4 + s / 4) * 64 + (e % 16) * 4 + s % 4
- * (the operand order of gfx950's 16x16x32 matrix instructions, so one page streams
- * as contiguous 1 KiB wave loads).  head_dim must be a multiple of 32.
+ *   K:  (((e / 32) * 2 + (s / 4) % 2) * 4 + (e % 32) / 8) * 64 + ((s / 8) * 4 + s % 4) * 8 + e % 8
+ *   V:  ((e / 16) * 2 + s / 8) * 128 + (e % 16) * 8 + s % 8
+ * (operand order of gfx950's 16x16x32 matrix instructions: a pair of pages streams as
+ * contiguous 512-byte half-wave loads, and every lane's K or V operand is one 16-byte
+ * load from one page).  head_dim must be a multiple of 32.
  * Token t of request i lives in block kv_page_table[i][t / 16], slot t % 16.
  */
 typedef struct {

@@ -203,6 +203,7 @@ def paged_attention(q, k_pool, v_pool, page_table, ctx_len, n_new, n_kv: int, bf
     documented K / V page layouts) as float32 or bf16 bits (uint16).  Returns [M][n_q][hd] fp64."""
     q = _c(q, np.float64)
     M, n_q, hd = q.shape
+    assert hd % 32 == 0, "the documented KV page layout needs head_dim % 32 == 0"
     out = np.empty_like(q)
     pt = _c(page_table, np.int32)
     ctx = _c(ctx_len, np.int32)
@@ -248,6 +249,7 @@ class OracleModel:
     arrays (fp32 model) or bf16 bit patterns (bf16 model)."""
 
     def __init__(self, shape, layers, glob):
+        assert shape.head_dim % 32 == 0, "the documented KV page layout needs head_dim % 32 == 0"
         self.shape = shape
         self.bf16 = shape.dtype == "bf16"
         self._keep = []

@@ -59,10 +59,12 @@ def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=Non
             Kn = _to_storage(K, s)
             Vn = _to_storage(V, s)
             if nf:
-                # K page: [dim/32][(dim%32)/8][slot][dim%8]; V page: [dim/16][slot/4][dim%16][slot%4]
-                k = Kn[:nf * wi.PAGE].reshape(nf, wi.PAGE, s.n_kv_heads, hd // 32, 4, 8)
-                kp[li, full] = k.transpose(0, 2, 3, 4, 1, 5).reshape(nf, s.n_kv_heads, -1)
-                v = Vn[:nf * wi.PAGE].reshape(nf, 4, 4, s.n_kv_heads, hd // 16, 16)
+                # whole pages by axis permutation (the layout's index tables, split into axes):
+                # K (slot s = 8a + 4b + c, dim e = 32f + 8g + h) sits at [f][b][g][a][c][h],
+                # V (slot s = 8a + c, dim e = 16f + h) sits at [f][a][h][c]
+                k = Kn[:nf * wi.PAGE].reshape(nf, 2, 2, 4, s.n_kv_heads, hd // 32, 4, 8)
+                kp[li, full] = k.transpose(0, 4, 5, 2, 6, 1, 3, 7).reshape(nf, s.n_kv_heads, -1)
+                v = Vn[:nf * wi.PAGE].reshape(nf, 2, 8, s.n_kv_heads, hd // 16, 16)
                 vp[li, full] = v.transpose(0, 3, 4, 1, 5, 2).reshape(nf, s.n_kv_heads, -1)
             if n > nf * wi.PAGE:
                 blk = page_table[i, nf]

@@ -374,7 +374,8 @@ static void rope(double *v, int hd, int pos, double base) {
 
 /* KV page layout for one layer: [n_blocks][n_kv][page], a page holding 16 slots x hd.
  * Inside a page, element (slot s, dim e) sits at
- *   K: ((e/32)*4 + (e%32)/8)*128 + s*8 + e%8      V: ((e/16)*4 + s/4)*64 + (e%16)*4 + s%4
+ *   K: (((e/32)*2 + (s/4)%2)*4 + (e%32)/8)*64 + ((s/8)*4 + s%4)*8 + e%8
+ *   V: ((e/16)*2 + s/8)*128 + (e%16)*8 + s%8
  * Token t of request i lives in block page_table[i][t / 16], slot t % 16. */
 static double kv_get(int bf16, const void *pool, int64_t idx) {
   return bf16 ? bf16_to_double(((const uint16_t *)pool)[idx]) : (double)((const float *)pool)[idx];
@@ -392,11 +393,12 @@ static int64_t page_base(int n_kv, int hd, int block, int kvh) {
 }
 
 static int64_t k_index(int n_kv, int hd, int block, int kvh, int slot, int dim) {
-  return page_base(n_kv, hd, block, kvh) + ((dim / 32) * 4 + (dim % 32) / 8) * 128 + slot * 8 + dim % 8;
+  return page_base(n_kv, hd, block, kvh) + (((dim / 32) * 2 + (slot / 4) % 2) * 4 + (dim % 32) / 8) * 64 +
+         ((slot / 8) * 4 + slot % 4) * 8 + dim % 8;
 }
 
 static int64_t v_index(int n_kv, int hd, int block, int kvh, int slot, int dim) {
-  return page_base(n_kv, hd, block, kvh) + ((dim / 16) * 4 + slot / 4) * 64 + (dim % 16) * 4 + slot % 4;
+  return page_base(n_kv, hd, block, kvh) + ((dim / 16) * 2 + slot / 8) * 128 + (dim % 16) * 8 + slot % 8;
 }
 
 /* Causal attention of the new rows over each request's paged KV (one layer).

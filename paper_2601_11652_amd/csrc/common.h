@@ -27,6 +27,13 @@ __device__ __forceinline__ uint32_t pack2bf(float a, float b) {
   return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
 }
 
+// the same rounding (nearest even) by gfx950's v_cvt_pk_bf16_f32, for finite values
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2bf_rne(float a, float b) {
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 template <typename T> struct Act;
 template <> struct Act<float> {
   static __device__ __forceinline__ float load(const float *p, int64_t i) { return p[i]; }
@@ -59,11 +66,14 @@ __device__ __forceinline__ uint4 keep_if(bool ok, uint4 v) {
 // ---------------------------------------------------------------------------------------
 // KV page layouts (one page = 16 slots x hd of one block and kv head)
 // ---------------------------------------------------------------------------------------
+// K: slots split by bit 2 into two groups of 8, each group's 32-dim chunk contiguous;
+// V: each dim's 8 consecutive slots contiguous (one 16-byte operand per lane)
 __device__ __forceinline__ int k_page_off(int slot, int e) {
-  return ((e >> 5) * 4 + ((e & 31) >> 3)) * 128 + slot * 8 + (e & 7);
+  return (((e >> 5) * 2 + ((slot >> 2) & 1)) * 4 + ((e & 31) >> 3)) * 64 + ((slot >> 3) * 4 + (slot & 3)) * 8 +
+         (e & 7);
 }
 __device__ __forceinline__ int v_page_off(int slot, int e) {
-  return ((e >> 4) * 4 + (slot >> 2)) * 64 + (e & 15) * 4 + (slot & 3);
+  return ((e >> 4) * 2 + (slot >> 3)) * 128 + (e & 15) * 8 + (slot & 7);
 }
 
 // Packed GEMM-operand layout: 32 x 16 fragments, fragment (rb, kb) of a matrix with K

@@ -55,7 +55,6 @@ struct Plan {
          w_rR = 0, total = 0;
 };
 
-constexpr int kAttnTargetItems = 1024;
 
 wisp_status check_model(const wisp_model *m, bool need_weights) {
   if (!m) return fail(WISP_E_INVALID, "model is NULL");
@@ -109,6 +108,15 @@ void carve(Plan &p, size_t &w, size_t &field, size_t bytes) {
 }
 
 // forward=true: the full step; false: acceptance only (rows/drafts of the batch, vocab V)
+// compute units of the current device (the attention work list is sized to them)
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  return n;
+}
+
 void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward, int vocab = 0) {
   p.B = d->B;
   p.V = forward ? m->vocab : vocab;
@@ -141,14 +149,28 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
       p.g_lm = gemm_bf16_plan(p.M, p.V, p.d);
       p.g_lm.splits = 1;
       p.g_lm.kf_per_split = p.d / 16;
-      // split-KV work list: items of <= 64 query rows and a chunk of page pairs
-      int64_t units = 0;
-      for (int i = 0; i < p.B; ++i) {
-        const int rows = (d->gamma[i] + 1) * p.G;
-        const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
-        units += (int64_t)nrbg * p.nkv * ((d->ctx_len[i] + d->gamma[i] + 1 + 31) / 32);
-      }
-      int chunk_pairs = (int)std::max<int64_t>(2, (units + kAttnTargetItems - 1) / kAttnTargetItems);
+      // split-KV work list: items of <= 48 query rows and a chunk of page pairs.  One wave
+      // per item and one 4-wave workgroup per CU are resident at a time, so the chunk is
+      // the shortest (of at most kAttnMaxChunkPages pages, whose block ids one wave keeps in
+      // a register) for which the items fill whole rounds of the device's wave slots: a
+      // round started by a few left-over workgroups would double the kernel's time.
+      const int64_t slots = 4 * (int64_t)device_cus();
+      auto count_items = [&](int cp) {
+        int64_t n = 0;
+        for (int i = 0; i < p.B; ++i) {
+          const int rows = (d->gamma[i] + 1) * p.G;
+          const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
+          const int64_t T = d->ctx_len[i] + d->gamma[i] + 1;
+          n += (int64_t)nrbg * p.nkv * ((T + 32 * cp - 1) / (32 * cp));
+        }
+        return n;
+      };
+      const int cp_max = kAttnMaxChunkPages / 2;
+      int64_t rounds = 1;
+      const int64_t fewest = count_items(cp_max);
+      while (rounds * slots < fewest) ++rounds;
+      int chunk_pairs = 2;
+      while (chunk_pairs < cp_max && count_items(chunk_pairs) > rounds * slots) ++chunk_pairs;
       const int chunk = 32 * chunk_pairs;
       for (int i = 0; i < p.B; ++i) {
         const int T = d->ctx_len[i] + d->gamma[i] + 1;
@@ -401,7 +423,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
     const int G = p.G;
     const int rows = (int)p.host[p.i_gamma + it.req] + 1;
     const int rbg = it.kvh_rbg >> 16;
-    const int nr = std::min(64, rows * G - rbg * 64);
+    const int nr = std::min(kAttnRowsPerItem, rows * G - rbg * kAttnRowsPerItem);
     if (rbg == 0) attn_bytes += (double)(it.t1 - it.t0) * kv_tok / p.nkv;
     attn_flops += 4.0 * p.hd * nr * (it.t1 - it.t0);
   }

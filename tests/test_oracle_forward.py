@@ -19,7 +19,7 @@ import wisp_inputs as wi
 from oracle import fixtures as fx
 
 MINI_BF16 = wi.ModelShape("mini-bf16-gqa", 2, 128, 4, 2, 32, 256, 512, "bf16", 10000.0)
-MINI_F32 = wi.ModelShape("mini-f32-gqa", 2, 128, 8, 2, 16, 192, 300, "f32", 10000.0)
+MINI_F32 = wi.ModelShape("mini-f32-gqa", 2, 128, 4, 2, 32, 192, 300, "f32", 10000.0)
 
 
 @pytest.fixture(scope="module", params=["tiny", "mini_bf16", "mini_f32"])

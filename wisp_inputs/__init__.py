@@ -200,17 +200,18 @@ def kv_values(seed: int, layer: int, req: int, start_pos: int, n_pos: int, n_kv:
 # KV page placement (the documented page layout; used to place inputs and read pages)
 # --------------------------------------------------------------------------------------
 def k_page_index(hd: int) -> np.ndarray:
-    """[16][hd] -> flat position inside a K page: ((e/32)*4 + (e%32)/8)*128 + s*8 + e%8."""
+    """[16][hd] -> flat position inside a K page:
+    (((e/32)*2 + (s/4)%2)*4 + (e%32)/8)*64 + ((s/8)*4 + s%4)*8 + e%8."""
     s = np.arange(PAGE)[:, None]
     e = np.arange(hd)[None, :]
-    return ((e // 32) * 4 + (e % 32) // 8) * 128 + s * 8 + e % 8
+    return (((e // 32) * 2 + (s // 4) % 2) * 4 + (e % 32) // 8) * 64 + ((s // 8) * 4 + s % 4) * 8 + e % 8
 
 
 def v_page_index(hd: int) -> np.ndarray:
-    """[16][hd] -> flat position inside a V page: ((e/16)*4 + s/4)*64 + (e%16)*4 + s%4."""
+    """[16][hd] -> flat position inside a V page: ((e/16)*2 + s/8)*128 + (e%16)*8 + s%8."""
     s = np.arange(PAGE)[:, None]
     e = np.arange(hd)[None, :]
-    return ((e // 16) * 4 + s // 4) * 64 + (e % 16) * 4 + s % 4
+    return ((e // 16) * 2 + s // 8) * 128 + (e % 16) * 8 + s % 8
 
 
 def pages_from_slots(x, which: str):
