@@ -59,3 +59,26 @@ def test_fit_report_protocol():
     assert rep["test"]["r2"] > 0.99
     m = LatencyModel.from_json(LatencyModel(**{k: rep["model"][k] for k in ("a", "b_compute", "b_read", "c")}).to_json())
     assert m.a == rep["model"]["a"]
+
+
+def test_sweep_configurations():
+    """The profiling sweep: 173 configurations in the five categories, deterministic,
+    gamma <= 16, and a disjoint 123 / 50 train / test split."""
+    from paper_2601_11652_amd import latency_sweep as ls
+    a = ls.sweep_configs()
+    b = ls.sweep_configs()
+    assert len(a) == 173
+    assert [(c.ctx_len, c.gamma) for c in a] == [(c.ctx_len, c.gamma) for c in b]
+    counts = {k: sum(c.category == k for c in a) for k in range(1, 6)}
+    assert counts == {1: 18, 2: 60, 3: 35, 4: 35, 5: 25}
+    for c in a:
+        assert len(c.ctx_len) == len(c.gamma) >= 1
+        assert max(c.gamma) <= 16 and min(c.gamma) >= 0 and min(c.ctx_len) >= 1
+    tr, te = ls.train_test_split(a)
+    assert len(tr) == 123 and len(te) == 50
+    assert not {c.cid for c in tr} & {c.cid for c in te}
+    X = ls.features(a)
+    assert X.shape == (173, 3) and np.all(np.isfinite(X))
+    # N_interactions >= N_linear (every new row sees at least itself), N_cached = sum ctx
+    assert np.all(X[:, 1] >= X[:, 0])
+    assert np.allclose(X[:, 2], [sum(c.ctx_len) for c in a])
