@@ -202,11 +202,14 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
     for (int i = 0; i < MT; ++i) acur[i] = lds[buf][(wm * MT + i) * R][lane];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      // activations of step r+1 are read from LDS while step r's products run
+      // activations of step r+1 are read from LDS while step r's products run (the
+      // barrier keeps the reads ahead of the products, in registers of their own, so the
+      // LDS latency is never exposed)
       if (r + 1 < R) {
 #pragma unroll
         for (int i = 0; i < MT; ++i) anext[i] = lds[buf][(wm * MT + i) * R + r + 1][lane];
       }
+      __builtin_amdgcn_sched_barrier(0);
       // consume ring slot r, then refill it: the slot's register is dead once the
       // products have issued, so no copy (and no early wait) is needed
 #pragma unroll
@@ -250,7 +253,7 @@ static constexpr int kKS = 4;
 // Launch plan.  M <= 256 (the verification step's sum(gamma+1) rows for the batch sizes
 // served here): weight-ring kernels that hold all of A per workgroup; wide outputs use
 // 64-column wave tiles (one A fragment feeds two products), narrow ones 32-column tiles
-// with a deeper ring.  K is split until about one workgroup per CU is in flight.
+// with a deeper ring.  K is split until one workgroup per CU is in flight (one round).
 // Larger M: the LDS-tiled kernel.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
@@ -272,8 +275,11 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
     R = kKS;
     tiles = ((N + c.bn - 1) / c.bn) * ((M + c.bm - 1) / c.bm);
   }
+  // workgroups resident at once: the ring kernels hold one workgroup per CU (LDS and
+  // registers), so more than one round of 256 would leave a partial second round
+  const int max_wg = c.kind == 0 ? 384 : 256;
   int splits = 1;
-  while (splits < 16 && tiles * splits * 2 <= 384 && KF / (splits * 2) >= 4 * R) splits *= 2;
+  while (splits < 16 && tiles * splits * 2 <= max_wg && KF / (splits * 2) >= 4 * R) splits *= 2;
   int kps = (KF + splits - 1) / splits;
   kps = (kps + R - 1) / R * R;
   c.splits = (KF + kps - 1) / kps;

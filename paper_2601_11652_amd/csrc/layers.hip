@@ -128,90 +128,151 @@ void embed_norm(const StepDesc &d, const T *embed, const T *gain, const int32_t 
   embed_norm_kernel<T><<<M, 256, dm * sizeof(float), s>>>(d, embed, gain, tokens, h, xn, packed, dm, V, eps);
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void resid_norm_kernel(const float *__restrict__ part, int splits,
-                                                         float *__restrict__ h,
-                                                         const T *__restrict__ gain,
-                                                         T *__restrict__ xn, bool packed, int M,
-                                                         int dm, float eps) {
-  __shared__ float sh[4];
-  extern __shared__ float row[];
-  const int r = blockIdx.x;
-  float *hr = h + (int64_t)r * dm;
-  for (int c = threadIdx.x * 4; c < dm; c += 256 * 4) {
-    const float4 acc = sum_splits4(part + (int64_t)r * dm + c, (int64_t)M * dm, splits);
-    float4 v = *reinterpret_cast<const float4 *>(hr + c);
-    v.x += acc.x;
-    v.y += acc.y;
-    v.z += acc.z;
-    v.w += acc.w;
-    *reinterpret_cast<float4 *>(hr + c) = v;
-    *reinterpret_cast<float4 *>(row + c) = v;
-  }
+// Fixed-order sum over the threads of a block of up to 1024 (waves reduce by shuffles,
+// then wave sums are added in wave order).
+__device__ __forceinline__ float block_sum(float v, float *sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6, nw = (blockDim.x + 63) >> 6;
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
   __syncthreads();
-  norm_store_row<T>(row, gain, xn, packed, r, dm, eps, sh);
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += sh[i];
+  return t;
+}
+
+// One row per workgroup, 8 columns per thread: every split partial and the residual are
+// loaded in one round, the new residual stays in registers for the norm.
+template <typename T>
+__global__ __launch_bounds__(1024) void resid_norm_kernel(const float *__restrict__ part, int splits,
+                                                          float *__restrict__ h,
+                                                          const T *__restrict__ gain,
+                                                          T *__restrict__ xn, bool packed, int M,
+                                                          int dm, float eps) {
+  __shared__ float sh[16];
+  const int r = blockIdx.x;
+  const int c = threadIdx.x * 8;
+  const bool on = c < dm;
+  float v[8];
+  float ss = 0.f;
+  if (on) {
+    const float *p = part + (int64_t)r * dm + c;
+    const int64_t stride = (int64_t)M * dm;
+    const float4 a0 = sum_splits4(p, stride, splits);
+    const float4 a1 = sum_splits4(p + 4, stride, splits);
+    float *hr = h + (int64_t)r * dm + c;
+    const float4 h0 = *reinterpret_cast<const float4 *>(hr);
+    const float4 h1 = *reinterpret_cast<const float4 *>(hr + 4);
+    v[0] = h0.x + a0.x; v[1] = h0.y + a0.y; v[2] = h0.z + a0.z; v[3] = h0.w + a0.w;
+    v[4] = h1.x + a1.x; v[5] = h1.y + a1.y; v[6] = h1.z + a1.z; v[7] = h1.w + a1.w;
+    *reinterpret_cast<float4 *>(hr) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4 *>(hr + 4) = make_float4(v[4], v[5], v[6], v[7]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
+  }
+  ss = block_sum(ss, sh);
+  if (!on) return;
+  const float inv = 1.0f / sqrtf(ss / (float)dm + eps);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = v[e] * inv * Act<T>::load(gain, c + e);
+  store8<T>(xn, packed, r, c, dm, v);
 }
 
 template <typename T>
 void resid_norm(const float *part, int splits, float *h, const T *gain, T *xn, bool packed, int M,
                 int dm, float eps, hipStream_t s) {
-  resid_norm_kernel<T><<<M, 256, dm * sizeof(float), s>>>(part, splits, h, gain, xn, packed, M, dm, eps);
+  const int threads = ((dm / 8 + 63) / 64) * 64;   // dm <= 8192
+  resid_norm_kernel<T><<<M, threads, 0, s>>>(part, splits, h, gain, xn, packed, M, dm, eps);
 }
 
 // ---------------------------------------------------------------------------------------
 // qkv partials -> RoPE (rotate-half) -> q buffer, k/v appended into the pages in place
 // ---------------------------------------------------------------------------------------
+// Grid (row, group of 8 heads); each thread owns 8 consecutive dims of one head.  The
+// rotate-half partner (dims i and i + hd/2) sits hd/16 lanes away and is exchanged with a
+// shuffle; q and K are written as 16-byte stores (8 consecutive dims are contiguous in
+// the K page layout), V element by element.
+constexpr int kRopeHeadsPerBlock = 8;
+
+template <typename T>
+__device__ __forceinline__ void store8_contig(T *p, const float *v);
+template <>
+__device__ __forceinline__ void store8_contig<float>(float *p, const float *v) {
+  *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4 *>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <>
+__device__ __forceinline__ void store8_contig<uint16_t>(uint16_t *p, const float *v) {
+  *reinterpret_cast<uint4 *>(p) = make_uint4(pack2bf(v[0], v[1]), pack2bf(v[2], v[3]),
+                                             pack2bf(v[4], v[5]), pack2bf(v[6], v[7]));
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void qkv_rope_append_kernel(StepDesc d, const float *__restrict__ part,
                                                               int splits, const float *__restrict__ cs,
                                                               T *__restrict__ q, T *__restrict__ k_pool,
                                                               T *__restrict__ v_pool, int M, int nq,
                                                               int nkv, int hd) {
-  extern __shared__ float row[];   // the row's summed q|k|v projections
   const int r = blockIdx.x;
-  const int N = (nq + 2 * nkv) * hd;
+  const int tph = hd / 8;                          // threads per head
+  const int head = blockIdx.y * kRopeHeadsPerBlock + threadIdx.x / tph;
+  const int nh = nq + 2 * nkv;
+  const int i0 = (threadIdx.x % tph) * 8;          // first dim of this thread
   const int h2 = hd / 2;
-  for (int c = threadIdx.x * 4; c < N; c += 256 * 4)
-    *reinterpret_cast<float4 *>(row + c) = sum_splits4(part + (int64_t)r * N + c, (int64_t)M * N, splits);
-  __syncthreads();
+  const int N = nh * hd;
+  float v[8];
+  if (head < nh) {
+    const float *p = part + (int64_t)r * N + head * hd + i0;
+    const int64_t stride = (int64_t)M * N;
+    const float4 a0 = sum_splits4(p, stride, splits);
+    const float4 a1 = sum_splits4(p + 4, stride, splits);
+    v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w;
+    v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
+  }
+  // rotate-half partner values (whole waves take part in the shuffle)
+  float w[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) w[e] = __shfl_xor(v[e], hd / 16);
+  if (head >= nh) return;
   const int req = d.row_req[r], pos = d.row_pos[r];
-  const int blk = d.page_table[(int64_t)req * d.pt_stride + pos / kPage];
-  const bool blk_ok = blk >= 0 && blk < d.n_blocks;
-  if (!blk_ok && threadIdx.x == 0) flag_error(d.err, kErrBlock);
-  const int slot = pos % kPage;
-  const int page_elems = kPage * hd;
-  const float *csr = cs + (int64_t)r * hd;   // [h2][2]
-  // rotated pairs (i, i + hd/2): q heads then k heads
-  for (int p = threadIdx.x; p < (nq + nkv) * h2; p += 256) {
-    const int head = p / h2, i = p % h2;
-    const float x1 = row[head * hd + i], x2 = row[head * hd + i + h2];
-    const float c = csr[2 * i], sn = csr[2 * i + 1];
-    const float y1 = x1 * c - x2 * sn;
-    const float y2 = x2 * c + x1 * sn;
-    if (head < nq) {
-      Act<T>::store(q, ((int64_t)r * nq + head) * hd + i, y1);
-      Act<T>::store(q, ((int64_t)r * nq + head) * hd + i + h2, y2);
-    } else if (blk_ok) {
-      const int kh = head - nq;
-      T *pg = k_pool + ((int64_t)blk * nkv + kh) * page_elems;
-      Act<T>::store(pg, k_page_off(slot, i), y1);
-      Act<T>::store(pg, k_page_off(slot, i + h2), y2);
+  if (head < nq + nkv) {   // RoPE on q and k heads
+    const float *csr = cs + (int64_t)r * hd;   // [h2][2]
+    const bool lo = i0 < h2;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = (lo ? i0 : i0 - h2) + e;
+      const float c = csr[2 * i], sn = csr[2 * i + 1];
+      v[e] = lo ? v[e] * c - w[e] * sn : v[e] * c + w[e] * sn;
     }
   }
-  if (blk_ok) {
-    for (int e = threadIdx.x; e < nkv * hd; e += 256) {
-      const int kh = e / hd, dim = e % hd;
-      T *pg = v_pool + ((int64_t)blk * nkv + kh) * page_elems;
-      Act<T>::store(pg, v_page_off(slot, dim), row[(nq + nkv) * hd + e]);
-    }
+  if (head < nq) {
+    store8_contig<T>(q + ((int64_t)r * nq + head) * hd + i0, v);
+    return;
+  }
+  const int blk = d.page_table[(int64_t)req * d.pt_stride + pos / kPage];
+  if (blk < 0 || blk >= d.n_blocks) {
+    if (threadIdx.x % tph == 0) flag_error(d.err, kErrBlock);
+    return;
+  }
+  const int slot = pos % kPage;
+  const int page_elems = kPage * hd;
+  if (head < nq + nkv) {
+    T *pg = k_pool + ((int64_t)blk * nkv + (head - nq)) * page_elems;
+    store8_contig<T>(pg + k_page_off(slot, i0), v);
+  } else {
+    T *pg = v_pool + ((int64_t)blk * nkv + (head - nq - nkv)) * page_elems;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) Act<T>::store(pg, v_page_off(slot, i0 + e), v[e]);
   }
 }
 
 template <typename T>
 void qkv_rope_append(const StepDesc &d, const float *part, int splits, const float *cs, T *q,
                      T *k_pool, T *v_pool, int M, int nq, int nkv, int hd, hipStream_t s) {
-  const int N = (nq + 2 * nkv) * hd;
-  qkv_rope_append_kernel<T><<<M, 256, N * sizeof(float), s>>>(d, part, splits, cs, q, k_pool, v_pool, M, nq, nkv, hd);
+  const int nh = nq + 2 * nkv;
+  dim3 grid(M, (nh + kRopeHeadsPerBlock - 1) / kRopeHeadsPerBlock);
+  qkv_rope_append_kernel<T><<<grid, kRopeHeadsPerBlock * hd / 8, 0, s>>>(d, part, splits, cs, q, k_pool, v_pool, M,
+                                                                        nq, nkv, hd);
 }
 
 // ---------------------------------------------------------------------------------------
