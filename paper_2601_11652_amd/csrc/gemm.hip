@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t *__restri
 // workgroup walks its K chunks in a rotated order.  The order is fixed per output tile,
 // so results stay deterministic.
 // ---------------------------------------------------------------------------------------
-template <int WM, int WN, int MT, int NT, int R>
+template <int WM, int WN, int MT, int NT, int R, int AD>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t *__restrict__ A,
                                                            const uint16_t *__restrict__ W,
                                                            float *__restrict__ C, int M, int N, int K,
@@ -139,14 +139,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
   const int MF = (M + 31) >> 5;
   const int kf0 = blockIdx.z * kf_per_split;
   const int kf1 = min(KF, kf0 + kf_per_split);
-  const int nch = (kf1 - kf0 + R - 1) / R;
+  // AD = 2: an even number of chunks (a chunk past the split reads zeroed activations)
+  const int nch = AD == 2 ? 2 * ((kf1 - kf0 + 2 * R - 1) / (2 * R)) : (kf1 - kf0 + R - 1) / R;
   const int rb0 = blockIdx.y * BMF;
   const int nbw = (blockIdx.x * WN + wn) * NT;   // this wave's first weight fragment
-  const int rot = nch > 0 ? (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)nch) : 0;
-  auto chunk_k = [&](int ch) {   // first K step of the ch-th chunk in this workgroup's order
-    int c = ch + rot;
-    c = c >= nch ? c - nch : c;
-    return kf0 + c * R;
+  const int rot = (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)nch);
+  auto chunk_k = [&](int ch) {   // first K step of the ch-th chunk in this workgroup's order;
+    return kf0 + ((ch + rot) % nch) * R;   // indices past the end wrap (loads never used)
   };
 
   floatx16 acc[MT][NT];
@@ -171,32 +170,33 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
 #pragma unroll
     for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, chunk_k(0) + r);
 
-  uint4 apre[A_PER_T];
-  auto aload = [&](int ch) {
+  // Activations reach LDS through register sets.  AD = 2: two sets, chunk c is loaded into
+  // set c % 2 two chunks before it is needed and written to LDS buffer c % 2 at the end of
+  // chunk c - 1, so an L2 round trip has two chunks of products to hide behind (measured
+  // better for the 64-column tiles, whose chunks are short).  AD = 1: one set, each chunk
+  // loaded one chunk ahead (measured better for the 32-column tiles).
+  static_assert(AD == 1 || AD == 2, "activation prefetch depth");
+  uint4 apre[AD][A_PER_T];
+  auto aload = [&](int set, int ch) {
 #pragma unroll
     for (int t = 0; t < A_PER_T; ++t) {
       const int c = tid + NTH * t;
       const int f = min(c >> 6, A_FR - 1), lc = c & 63;
       const int r = rb0 + f / R, kf = chunk_k(ch) + f % R;
       const bool ok = r < MF && kf < kf1;
-      apre[t] = keep_if(ok, ld16(A + (((int64_t)(ok ? r : 0) * KF + (ok ? kf : 0)) * 64 + lc) * 8));
+      apre[set][t] = keep_if(ok, ld16(A + (((int64_t)(ok ? r : 0) * KF + (ok ? kf : 0)) * 64 + lc) * 8));
     }
   };
-  auto astore = [&](int buf) {
+  auto astore = [&](int set, int buf) {
 #pragma unroll
     for (int t = 0; t < A_PER_T; ++t) {
       const int c = tid + NTH * t;
-      if (c < A_FR * 64) lds[buf][c >> 6][c & 63] = apre[t];
+      if (c < A_FR * 64) lds[buf][c >> 6][c & 63] = apre[set][t];
     }
   };
-
-  aload(0);
-  astore(0);
-  __syncthreads();
-  if (nch > 1) aload(1);
-  for (int ch = 0; ch < nch; ++ch) {
-    const int buf = ch & 1;
-    const int kn = chunk_k(ch + 1 < nch ? ch + 1 : ch);   // next chunk (last: a harmless reload)
+  // one chunk of R K steps from LDS buffer `buf`, refilling the ring from chunk ch + 1
+  auto chunk = [&](int buf, int ch) {
+    const int kn = chunk_k(ch + 1);
     uint4 acur[MT], anext[MT];
 #pragma unroll
     for (int i = 0; i < MT; ++i) acur[i] = lds[buf][(wm * MT + i) * R][lane];
@@ -226,9 +226,36 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
       }
       __builtin_amdgcn_sched_barrier(0);   // keep each refill right after its slot's use
     }
-    if (ch + 1 < nch) astore(buf ^ 1);
+  };
+
+  if constexpr (AD == 2) {
+    aload(0, 0);
+    astore(0, 0);
     __syncthreads();
-    if (ch + 2 < nch) aload(ch + 2);
+    aload(1, 1);
+    aload(0, 2);
+    for (int ch = 0; ch < nch; ch += 2) {   // straight-line body: every load unconditional
+      chunk(0, ch);
+      astore(1, 1);       // chunk ch + 1
+      __syncthreads();
+      aload(1, ch + 3);
+      chunk(1, ch + 1);
+      astore(0, 0);       // chunk ch + 2
+      __syncthreads();
+      aload(0, ch + 4);
+    }
+  } else {
+    aload(0, 0);
+    astore(0, 0);
+    __syncthreads();
+    if (nch > 1) aload(0, 1);
+    for (int ch = 0; ch < nch; ++ch) {
+      const int buf = ch & 1;
+      chunk(buf, ch);
+      if (ch + 1 < nch) astore(0, buf ^ 1);
+      __syncthreads();
+      if (ch + 2 < nch) aload(0, ch + 2);
+    }
   }
 
   float *Cz = C + (int64_t)blockIdx.z * M * ldc;
@@ -249,6 +276,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
 }
 
 static constexpr int kKS = 4;
+static constexpr int kNarrowAD = 1;   // activation prefetch depth of the 32-column ring
 
 // Launch plan.  M <= 256 (the verification step's sum(gamma+1) rows for the batch sizes
 // served here): weight-ring kernels that hold all of A per workgroup; wide outputs use
@@ -287,12 +315,12 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   return c;
 }
 
-template <int NT, int R>
+template <int NT, int R, int AD>
 static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W, float *C, int M,
                         int N, int K, int ldc, int kps, hipStream_t s) {
   switch (mt) {
 #define WISP_RING_CASE(X) \
-  case X: gemm_ring_kernel<1, 4, X, NT, R><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, kps); break;
+  case X: gemm_ring_kernel<1, 4, X, NT, R, AD><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, kps); break;
     WISP_RING_CASE(1)
     WISP_RING_CASE(2)
     WISP_RING_CASE(3)
@@ -314,9 +342,9 @@ void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int
   }
   dim3 grid((N + cfg.bn - 1) / cfg.bn, 1, cfg.splits);
   if (cfg.kind == 1)
-    launch_ring<1, 8>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+    launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
   else
-    launch_ring<2, 4>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+    launch_ring<2, 4, 2>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
 }
 
 // ---------------------------------------------------------------------------------------
