@@ -6,7 +6,8 @@
 // bf16 path, one wave per work item (request, kv head, group of <= 48 query rows, token
 // chunk).  Per 32 tokens (a page pair) the wave computes S^T = K Q^T and O^T += V^T P^T
 // with v_mfma_f32_16x16x32_bf16.  Computing the transposed products keeps every query row
-// in one lane column (lane % 16), so the online softmax needs only two cross-lane steps,
+// in one lane column (lane % 16), so the online softmax needs only two cross-row steps
+// (VALU lane swaps),
 // and the probabilities leave the first product in exactly the register order the second
 // one consumes.  The token order inside the pair is chosen (through the K and V page
 // layouts) so that lane group g = lane / 16 holds tokens 8g .. 8g + 7 of the pair, all in
@@ -143,8 +144,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
       }
       float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
                        fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = xor32_max(xor16_max(mx));
       const bool grow = mx > m_run[rb] + tau_raw;   // false while the row has seen no token
       if (__builtin_amdgcn_ballot_w64(grow)) {      // wave-uniform: some row raises its max
         const float alpha = grow ? __builtin_amdgcn_exp2f((m_run[rb] - mx) * c_log2) : 1.0f;
@@ -167,8 +167,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
           pw[h * 2 + e / 2] = pk;
           rs += __uint_as_float(pk << 16) + __uint_as_float(pk & 0xFFFF0000u);
         }
-      rs += __shfl_xor(rs, 16);
-      rs += __shfl_xor(rs, 32);
+      rs = xor32_sum(xor16_sum(rs));
       l_run[rb] += rs;
       const bf16x8_t pb = as_bf16x8(make_uint4(pw[0], pw[1], pw[2], pw[3]));
 #pragma unroll

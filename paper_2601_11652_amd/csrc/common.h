@@ -64,6 +64,30 @@ __device__ __forceinline__ uint4 keep_if(bool ok, uint4 v) {
 }
 
 // ---------------------------------------------------------------------------------------
+// Cross-row reductions of a wave (rows = 16-lane groups) on the VALU: gfx950's
+// v_permlane16_swap / v_permlane32_swap exchange rows between two registers, so combining
+// both outputs reduces over lanes l and l ^ 16 (or l ^ 32) without a trip through LDS.
+// Each lane ends with the same value as a shuffle-based reduction (the pairwise
+// combination is commutative).
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ float xor16_max(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor16_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ---------------------------------------------------------------------------------------
 // KV page layouts (one page = 16 slots x hd of one block and kv head)
 // ---------------------------------------------------------------------------------------
 // K: slots split by bit 2 into two groups of 8, each group's 32-dim chunk contiguous;

@@ -1,0 +1,155 @@
+"""Edge cases of the verification step on the GPU, each against the oracle.
+
+* an empty batch is a no-op (outputs untouched);
+* requests with no cached context (ctx_len = 0: the rows attend only to each other),
+  single-token contexts and the longest draft (gamma = 16) next to plain-decode requests
+  (gamma = 0), on the fp32 model (1e-4 relative per row) and the bf16 model (2e-2
+  max-abs);
+* a batch of plain-decode requests only (no draft rows; the draft distributions may be
+  NULL);
+* more than 256 rows (24 requests x 17 rows = 408), which takes the LDS-tiled GEMM path;
+* an out-of-range block id in the page table: the kernels clamp it, write nothing through
+  it, and wisp_check reports a device input error.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2601_11652_amd as W
+import wisp_inputs as wi
+from oracle import fixtures as fx
+from gpu_harness import Workload, compare_decisions, gpu_model, log, rel_row_err, run_gpu, storage_to_f64, to_dev
+
+pytestmark = pytest.mark.gpu
+
+MINI_BF16 = wi.ModelShape("mini-bf16-gqa", 2, 256, 8, 2, 64, 512, 1024, "bf16", 10000.0)
+
+
+def _check_written(wl, pools_gpu, atol):
+    mix = wl.mix
+    hd = mix.shape.head_dim
+    for which, idx_fn in ((0, wi.k_page_index), (1, wi.v_page_index)):
+        g = storage_to_f64(pools_gpu[which])
+        r = storage_to_f64(wl.pools_ref[which])
+        before = storage_to_f64(wl.pools0[which])
+        written = np.zeros(g.shape, bool)
+        idx = idx_fn(hd)
+        for i in range(mix.B):
+            for pos in range(mix.ctx_len[i], mix.ctx_len[i] + mix.gamma[i] + 1):
+                written[:, wl.pt[i, pos // 16], :, idx[pos % 16]] = True
+        assert np.abs(g[written] - r[written]).max() <= atol
+        np.testing.assert_array_equal(g[~written], before[~written])
+
+
+def _run_case(shape, ctx, gamma, logit_check, kv_atol, u_margin=1e-3):
+    mix = wi.custom_mix(shape, ctx, gamma, kv_source="prefill", name="edge", t_draft=1.0, sigma=0.5)
+    log(f"{shape.name}: ctx={list(ctx)} gamma={list(gamma)} (M = {mix.M})")
+    model = fx.host_model(shape)
+    wl = Workload(mix, model)
+    gm = gpu_model(shape)
+    acc, out, logits, pools = run_gpu(gm, wl)
+    logit_check(logits, wl.logits_ref)
+    _check_written(wl, pools, kv_atol)
+    ref = oracle.accept(wl.logits_ref, wl.tokens, wl.q, mix.gamma, 1.0, wl.seed, req_id=mix.req_id)
+    gap = float(np.abs(logits - wl.logits_ref).max())
+    n_dec, mism, unflagged = compare_decisions(acc, out, ref, mix.gamma, wl.tokens, u_margin, 1e-3,
+                                               residual_exempt=shape.dtype == "bf16", logit_gap=gap)
+    log(f"  decisions {n_dec}, mismatches {mism}, unflagged {unflagged}")
+    assert not unflagged
+
+
+def _fp32_rows(logits, ref):
+    err = rel_row_err(logits, ref)
+    log(f"  max relative row error {err.max():.2e}")
+    assert err.max() <= 1e-4
+
+
+def _bf16_abs(logits, ref):
+    d = np.abs(logits - ref).max()
+    log(f"  max-abs logits error {d:.3e}")
+    assert d <= 2e-2
+
+
+def test_empty_batch_is_a_no_op():
+    shape = wi.TINY
+    gm = gpu_model(shape)
+    kv = W.KVPool.zeros(shape.n_layers, 4, shape.n_kv_heads, shape.head_dim, torch.float32)
+    pt = torch.zeros((0, 1), dtype=torch.int32, device="cuda")
+    desc = W.BatchDesc(np.zeros(0, np.int32), np.zeros(0, np.int32), pt, 1.0)
+    ws = W.workspace(max(256, W.wisp_workspace_size(gm.c, desc)))
+    sentinel = torch.full((4,), -7, dtype=torch.int32, device="cuda")
+    logits = torch.full((4,), 3.0, device="cuda")
+    W.wisp_verify(gm.c, kv, desc, sentinel, None, 1, sentinel, sentinel, logits, ws)
+    torch.cuda.synchronize()
+    assert torch.all(sentinel == -7) and torch.all(logits == 3.0)
+    assert torch.all(kv.k == 0) and torch.all(kv.v == 0)
+
+
+@pytest.mark.parametrize("shape,check,kv_atol", [(wi.TINY, _fp32_rows, 1e-4), (MINI_BF16, _bf16_abs, 6e-2)],
+                         ids=["fp32", "bf16"])
+def test_zero_and_short_contexts_with_longest_drafts(shape, check, kv_atol):
+    _run_case(shape, [0, 0, 1, 15, 16, 33], [3, 0, 16, 16, 0, 7], check, kv_atol)
+
+
+@pytest.mark.parametrize("shape,check,kv_atol", [(wi.TINY, _fp32_rows, 1e-4), (MINI_BF16, _bf16_abs, 6e-2)],
+                         ids=["fp32", "bf16"])
+def test_plain_decode_batch_without_draft_rows(shape, check, kv_atol):
+    mix = wi.custom_mix(shape, [5, 40, 0, 17], [0, 0, 0, 0], kv_source="prefill", name="decode")
+    log(f"{shape.name}: plain decode, ctx={list(mix.ctx_len)}")
+    model = fx.host_model(shape)
+    wl = Workload(mix, model)
+    gm = gpu_model(shape)
+    kv = W.KVPool(to_dev(wl.pools0[0]), to_dev(wl.pools0[1]))
+    desc = W.BatchDesc(mix.ctx_len, mix.gamma, to_dev(wl.pt), 1.0, mix.req_id)
+    ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
+    acc = torch.full((mix.B,), -7, dtype=torch.int32, device="cuda")
+    out = torch.full((mix.M,), -7, dtype=torch.int32, device="cuda")
+    logits = torch.empty(mix.M, shape.vocab, dtype=torch.float32, device="cuda")
+    W.wisp_verify(gm.c, kv, desc, to_dev(wl.tokens), None, wl.seed, acc, out, logits, ws)   # NULL q
+    W.wisp_check(ws)
+    torch.cuda.synchronize()
+    check(logits.cpu().numpy(), wl.logits_ref)
+    ref = oracle.accept(wl.logits_ref, wl.tokens, wl.q, mix.gamma, 1.0, wl.seed, req_id=mix.req_id)
+    assert np.all(acc.cpu().numpy() == 0)
+    # gamma = 0: the one output token is a draw from p; identical unless the race is a near tie
+    o = out.cpu().numpy()
+    gap = float(np.abs(logits.cpu().numpy() - wl.logits_ref).max())
+    for i in range(mix.B):
+        if o[i] != ref.out_tokens[i]:
+            assert abs(ref.race_key1[i] - ref.race_key2[i]) < 1e-3 + 4 * gap, (i, o[i], ref.out_tokens[i])
+
+
+def test_more_than_256_rows_takes_the_tiled_gemm():
+    B = 24
+    ctx = [int(c) for c in np.random.default_rng(5).integers(0, 96, size=B)]
+    _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs, 6e-2)
+
+
+def test_out_of_range_block_id_is_reported():
+    shape = wi.TINY
+    mix = wi.custom_mix(shape, [20, 40], [2, 3], name="badblock")
+    pt_np, nb = wi.page_table(mix)
+    bad = pt_np.copy()
+    bad[1, 1] = nb + 1000                 # a context page of request 1
+    bad[0, 1] = nb                        # the page request 0's new rows are written to
+    gm = gpu_model(shape)
+    kv = W.KVPool.zeros(shape.n_layers, nb, shape.n_kv_heads, shape.head_dim, torch.float32)
+    desc = W.BatchDesc(mix.ctx_len, mix.gamma, to_dev(bad), 1.0)
+    ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
+    tokens = torch.zeros(mix.M, dtype=torch.int32, device="cuda")
+    q = torch.full((int(mix.gamma.sum()), shape.vocab), 1.0 / shape.vocab, device="cuda")
+    acc = torch.empty(mix.B, dtype=torch.int32, device="cuda")
+    out = torch.empty(mix.M, dtype=torch.int32, device="cuda")
+    logits = torch.empty(mix.M, shape.vocab, device="cuda")
+    W.wisp_verify(gm.c, kv, desc, tokens, q, 3, acc, out, logits, ws)
+    with pytest.raises(W.WispError) as e:
+        W.wisp_check(ws)
+    assert "block id" in str(e.value)
+    # nothing was written through the invalid ids: the pool stays finite, and the first
+    # call after the report starts clean
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(kv.k).all()) and bool(torch.isfinite(kv.v).all())
+    good = W.BatchDesc(mix.ctx_len, mix.gamma, to_dev(pt_np), 1.0)
+    W.wisp_verify(gm.c, kv, good, tokens, q, 3, acc, out, logits, ws)
+    W.wisp_check(ws)
