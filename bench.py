@@ -8,8 +8,9 @@ q = softmax(logits / T + N(0, 0.5)) with T ~ U[0.8, 1.2] per request.
 
 One step = one wisp_verify call: forward of all sum(gamma+1) rows over the paged KV plus
 acceptance.  Inputs are resident in HBM before timing; the call is idempotent, so the
-same batch is verified W + K times.  Metric: committed (accepted + extra) tokens per
-second, sum(L_i + 1) / step time, with the step latency alongside.
+same batch is verified W + K times, each time with its own acceptance seed.  Metric:
+committed (accepted + extra) tokens per second, sum(L_i + 1) averaged over the K timed
+steps' draws / step time, with the step latency alongside.
 
 Prints ONE JSON line.  Also reports the dominant kernel class against its roofline
 (algorithmic bytes per launch over the HIP-event-timed average launch) and the CPU
@@ -31,7 +32,7 @@ HBM_PEAK_GBS = 8000.0
 # timing classes of the library's profiling hook (include/wisp.h) and the kernels they cover
 KERNEL_CLASSES = ((0, "gemm_ring1"), (1, "gemm_ring2"), (2, "gemm_tiled"), (3, "attention"),
                   (4, "attention_combine"), (5, "rows"), (6, "sampler"))
-KERNEL_NAMES = {"gemm_ring1": "gemm_ring_kernel<1, 4, MT, 1, 8>", "gemm_ring2": "gemm_ring_kernel<1, 4, MT, 2, 4>",
+KERNEL_NAMES = {"gemm_ring1": "gemm_ring_kernel<1, 4, MT, 1, 8, 1>", "gemm_ring2": "gemm_ring_kernel<1, 4, MT, 2, 4, 2>",
                 "gemm_tiled": "gemm_bf16_kernel", "attention": "attn_bf16_kernel",
                 "attention_combine": "attn_combine_kernel", "rows": "row kernels", "sampler": "sampler kernels"}
 BF16_PEAK_TFLOPS = 2516.6
@@ -169,31 +170,33 @@ def main():
     desc = W.BatchDesc(mix.ctx_len, mix.gamma, pt, 1.0, mix.req_id)
     ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
     M = mix.M
-    acc = torch.empty(mix.B, dtype=torch.int32, device="cuda")
+    # every timed step draws its own acceptance randomness (seed + step) into its own row of
+    # accepted lengths, so the committed-token count is a mean over the K steps' draws
+    accs = torch.empty((args.warmup + args.steps, mix.B), dtype=torch.int32, device="cuda")
     out = torch.empty(M, dtype=torch.int32, device="cuda")
     logits = torch.empty(M, s.vocab, dtype=torch.float32, device="cuda")
     seed = wi.verify_seed(mix)
 
-    def step():
-        W.wisp_verify(gm.c, kv, desc, tokens, q, seed, acc, out, logits, ws)
+    def step(i=0):
+        W.wisp_verify(gm.c, kv, desc, tokens, q, seed + i, accs[i], out, logits, ws)
 
-    for _ in range(args.warmup):
-        step()
+    for i in range(args.warmup):
+        step(i)
     W.wisp_check(ws)
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
-    for _ in range(args.steps):
-        step()
+    for i in range(args.warmup, args.warmup + args.steps):
+        step(i)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = e0.elapsed_time(e1) / args.steps
     log(f"{args.steps} steps: {ms_step:.3f} ms/step (events), {wall / args.steps * 1e3:.3f} ms/step (wall)")
-    L = acc.cpu().numpy()
-    committed = int((L + 1).sum())
+    L = accs[args.warmup:].cpu().numpy().astype(np.int64)
+    committed = float((L + 1).sum()) / args.steps
     value = committed / (ms_step / 1e3)
 
     # per-kernel-class durations: HIP events around each launch on the library's stream
@@ -250,8 +253,8 @@ def main():
         "config": {"workload": f"{args.config}: {s.name} verification step", "B": mix.B, "rows": M,
                    "sum_ctx": int(mix.ctx_len.sum()), "sum_gamma": int(mix.gamma.sum()), "page": 16,
                    "layers": s.n_layers, "vocab": s.vocab},
-        "accepted_drafts_per_s": int(L.sum()) / (ms_step / 1e3),
-        "acceptance_rate": float(L.sum()) / max(1, int(mix.gamma.sum())),
+        "accepted_drafts_per_s": float(L.sum()) / args.steps / (ms_step / 1e3),
+        "acceptance_rate": float(L.sum()) / args.steps / max(1, int(mix.gamma.sum())),
         "committed_tokens_per_step": committed,
         "roofline": roof,
         "kernels": classes,

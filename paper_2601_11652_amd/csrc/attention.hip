@@ -300,9 +300,9 @@ void attention_bf16_main(const StepDesc &d, const AttnItem *items, int n_items, 
   constexpr int RB = kAttnRowsPerItem / 16;
   constexpr int kAttnRing = 2;   // page pairs in registers: one computed, one loading
   if (hd == 128)
-    attn_bf16_kernel<128, RB, kAttnRing><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
+    launch(attn_bf16_kernel<128, RB, kAttnRing>, blocks, 256, 0, s, d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
   else
-    attn_bf16_kernel<64, RB, kAttnRing><<<blocks, 256, 0, s>>>(d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
+    launch(attn_bf16_kernel<64, RB, kAttnRing>, blocks, 256, 0, s, d, items, n_items, q, k_pool, v_pool, part_o, part_ml, nq, nkv, scale);
 }
 
 void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_groups,
@@ -312,11 +312,11 @@ void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_gr
   constexpr int kMaxC = 8;
   if (hd == 128) {
     const int64_t threads = (int64_t)n_groups * kAttnRowsPerItem * 16;
-    attn_combine_kernel<128, kMaxC><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(
+    launch(attn_combine_kernel<128, kMaxC>, (unsigned)((threads + 255) / 256), 256, 0, s,
         d, groups, n_groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
   } else {
     const int64_t threads = (int64_t)n_groups * kAttnRowsPerItem * 8;
-    attn_combine_kernel<64, kMaxC><<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(
+    launch(attn_combine_kernel<64, kMaxC>, (unsigned)((threads + 255) / 256), 256, 0, s,
         d, groups, n_groups, part_o, part_ml, out, out_packed, out_K, nq, nkv);
   }
 }
@@ -391,7 +391,7 @@ void attention_f32(const StepDesc &d, int B, const float *q, const float *k_pool
                    const float *v_pool, float *out, int nq, int nkv, int hd, int max_tokens,
                    hipStream_t s) {
   const float scale = 1.0f / sqrtf((float)hd);
-  attn_f32_kernel<<<B * nq, 256, max_tokens * sizeof(float), s>>>(d, q, k_pool, v_pool, out, nq, nkv, hd, scale);
+  launch(attn_f32_kernel, B * nq, 256, max_tokens * sizeof(float), s, d, q, k_pool, v_pool, out, nq, nkv, hd, scale);
 }
 
 }  // namespace wisp

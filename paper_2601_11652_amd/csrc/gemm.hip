@@ -137,13 +137,20 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
   const int wm = wave / WN, wn = wave % WN;
   const int KF = K >> 4, NF = N >> 5;
   const int MF = (M + 31) >> 5;
-  const int kf0 = blockIdx.z * kf_per_split;
+  // a 1-D grid of (output tile, K split) pairs.  Workgroups are dealt to the 8 XCDs in
+  // turn (linear id mod 8), so taking the split from the low digits of the id keeps each
+  // split's workgroups on as few XCDs as possible: every XCD's L2 then fetches only the
+  // activation columns of its own K ranges instead of all of them
+  const int splits = (KF + kf_per_split - 1) / kf_per_split;
+  const int zs = (int)(blockIdx.x % (unsigned)splits);
+  const int tile = (int)(blockIdx.x / (unsigned)splits);
+  const int kf0 = zs * kf_per_split;
   const int kf1 = min(KF, kf0 + kf_per_split);
   // AD = 2: an even number of chunks (a chunk past the split reads zeroed activations)
   const int nch = AD == 2 ? 2 * ((kf1 - kf0 + 2 * R - 1) / (2 * R)) : (kf1 - kf0 + R - 1) / R;
   const int rb0 = blockIdx.y * BMF;
-  const int nbw = (blockIdx.x * WN + wn) * NT;   // this wave's first weight fragment
-  const int rot = (int)((blockIdx.x * 7u + blockIdx.y * 3u) % (unsigned)nch);
+  const int nbw = (tile * WN + wn) * NT;   // this wave's first weight fragment
+  const int rot = (int)(((unsigned)tile * 7u + blockIdx.y * 3u) % (unsigned)nch);
   auto chunk_k = [&](int ch) {   // first K step of the ch-th chunk in this workgroup's order;
     return kf0 + ((ch + rot) % nch) * R;   // indices past the end wrap (loads never used)
   };
@@ -258,7 +265,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
     }
   }
 
-  float *Cz = C + (int64_t)blockIdx.z * M * ldc;
+  float *Cz = C + (int64_t)zs * M * ldc;
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
     const int rbase = (rb0 + wm * MT + i) * 32 + 4 * (lane >> 5);
@@ -320,7 +327,7 @@ static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W,
                         int N, int K, int ldc, int kps, hipStream_t s) {
   switch (mt) {
 #define WISP_RING_CASE(X) \
-  case X: gemm_ring_kernel<1, 4, X, NT, R, AD><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, kps); break;
+  case X: launch(gemm_ring_kernel<1, 4, X, NT, R, AD>, grid, 256, 0, s, A, W, C, M, N, K, ldc, kps); break;
     WISP_RING_CASE(1)
     WISP_RING_CASE(2)
     WISP_RING_CASE(3)
@@ -337,10 +344,10 @@ void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int
                const GemmCfg &cfg, hipStream_t s) {
   if (cfg.kind == 0) {
     dim3 grid((N + cfg.bn - 1) / cfg.bn, (M + cfg.bm - 1) / cfg.bm, cfg.splits);
-    gemm_bf16_kernel<2, 2, 4, 2, kKS><<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc, cfg.kf_per_split);
+    launch(gemm_bf16_kernel<2, 2, 4, 2, kKS>, grid, 256, 0, s, A, W, C, M, N, K, ldc, cfg.kf_per_split);
     return;
   }
-  dim3 grid((N + cfg.bn - 1) / cfg.bn, 1, cfg.splits);
+  dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, 1, 1);
   if (cfg.kind == 1)
     launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
   else
@@ -389,7 +396,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
 
 void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int ldc, hipStream_t s) {
   dim3 grid((N + 63) / 64, (M + 31) / 32, 1);
-  gemm_f32_kernel<<<grid, 256, 0, s>>>(A, W, C, M, N, K, ldc);
+  launch(gemm_f32_kernel, grid, 256, 0, s, A, W, C, M, N, K, ldc);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -411,7 +418,7 @@ void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hi
   const int64_t chunks = (int64_t)rows * (cols / 8);
   int blocks = (int)((chunks + 255) / 256);
   if (blocks > 65535) blocks = 65535;
-  pack_bf16_kernel<<<blocks, 256, 0, s>>>(dst, src, rows, cols);
+  launch(pack_bf16_kernel, blocks, 256, 0, s, dst, src, rows, cols);
 }
 
 }  // namespace wisp

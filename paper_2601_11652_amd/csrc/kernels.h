@@ -1,9 +1,26 @@
 // Host-side launchers of the gfx950 kernels (one translation unit per kernel family).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace wisp {
+
+// ----- kernel launch ---------------------------------------------------------------------
+// While per-launch timing is on, launch_timing_events hands out a pair of HIP events and the
+// launch goes through hipExtLaunchKernelGGL, which stamps them with the dispatch's own begin
+// and end (the gap between dispatches is not counted); otherwise it is a plain launch.
+bool launch_timing_events(hipEvent_t *start, hipEvent_t *stop);
+
+template <typename... Formals, typename... Actuals>
+inline void launch(void (*kernel)(Formals...), dim3 grid, dim3 block, uint32_t shm, hipStream_t s,
+                   Actuals... args) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (launch_timing_events(&a, &b))
+    hipExtLaunchKernelGGL(kernel, grid, block, shm, s, a, b, 0u, args...);
+  else
+    kernel<<<grid, block, shm, s>>>(args...);
+}
 
 // ----- GEMMs: C[z][M][ldc] (fp32) = A[M][K] . W[N][K]^T over the z-th K range ----------
 struct GemmCfg {

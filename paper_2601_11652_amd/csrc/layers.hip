@@ -76,7 +76,7 @@ __global__ void rope_table_kernel(const int32_t *__restrict__ row_pos, float *__
 
 void rope_table(const StepDesc &d, float *cs, int M, int hd, float base, hipStream_t s) {
   const int n = M * hd / 2;
-  rope_table_kernel<<<(n + 255) / 256, 256, 0, s>>>(d.row_pos, cs, M, hd, base);
+  launch(rope_table_kernel, (n + 255) / 256, 256, 0, s, d.row_pos, cs, M, hd, base);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -125,7 +125,7 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(StepDesc d, const T *__
 template <typename T>
 void embed_norm(const StepDesc &d, const T *embed, const T *gain, const int32_t *tokens, float *h,
                 T *xn, bool packed, int M, int dm, int V, float eps, hipStream_t s) {
-  embed_norm_kernel<T><<<M, 256, dm * sizeof(float), s>>>(d, embed, gain, tokens, h, xn, packed, dm, V, eps);
+  launch(embed_norm_kernel<T>, M, 256, dm * sizeof(float), s, d, embed, gain, tokens, h, xn, packed, dm, V, eps);
 }
 
 // Fixed-order sum over the threads of a block of up to 1024 (waves reduce by shuffles,
@@ -182,7 +182,7 @@ template <typename T>
 void resid_norm(const float *part, int splits, float *h, const T *gain, T *xn, bool packed, int M,
                 int dm, float eps, hipStream_t s) {
   const int threads = ((dm / 8 + 63) / 64) * 64;   // dm <= 8192
-  resid_norm_kernel<T><<<M, threads, 0, s>>>(part, splits, h, gain, xn, packed, M, dm, eps);
+  launch(resid_norm_kernel<T>, M, threads, 0, s, part, splits, h, gain, xn, packed, M, dm, eps);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -271,7 +271,7 @@ void qkv_rope_append(const StepDesc &d, const float *part, int splits, const flo
                      T *k_pool, T *v_pool, int M, int nq, int nkv, int hd, hipStream_t s) {
   const int nh = nq + 2 * nkv;
   dim3 grid(M, (nh + kRopeHeadsPerBlock - 1) / kRopeHeadsPerBlock);
-  qkv_rope_append_kernel<T><<<grid, kRopeHeadsPerBlock * hd / 8, 0, s>>>(d, part, splits, cs, q, k_pool, v_pool, M,
+  launch(qkv_rope_append_kernel<T>, grid, kRopeHeadsPerBlock * hd / 8, 0, s, d, part, splits, cs, q, k_pool, v_pool, M,
                                                                         nq, nkv, hd);
 }
 
@@ -306,7 +306,7 @@ void swiglu(const float *part, int splits, T *out, bool packed, int M, int F, hi
   const int64_t chunks = (int64_t)M * (F / 8);
   int blocks = (int)((chunks + 255) / 256);
   if (blocks > 4096) blocks = 4096;
-  swiglu_kernel<T><<<blocks, 256, 0, s>>>(part, splits, out, packed, M, F);
+  launch(swiglu_kernel<T>, blocks, 256, 0, s, part, splits, out, packed, M, F);
 }
 
 template void embed_norm<float>(const StepDesc &, const float *, const float *, const int32_t *,

@@ -285,11 +285,11 @@ void sampler(const StepDesc &d, int B, int M, int V, const float *logits, const 
              int32_t *out_tokens, hipStream_t s) {
   if (B == 0) return;
   const int CH = sampler_chunks(V);
-  row_max_kernel<<<dim3(M, CH), 256, 0, s>>>(logits, V, T, CH, sc.part_m, sc.part_i);
-  if (T != 0.f) row_sum_kernel<<<dim3(M, CH), 256, 0, s>>>(logits, V, T, CH, sc.part_m, sc.part_s);
-  race_kernel<<<dim3(B, CH), 256, 0, s>>>(d, V, logits, tokens, q, T, seed, CH, sc.part_m, sc.part_i,
+  launch(row_max_kernel, dim3(M, CH), 256, 0, s, logits, V, T, CH, sc.part_m, sc.part_i);
+  if (T != 0.f) launch(row_sum_kernel, dim3(M, CH), 256, 0, s, logits, V, T, CH, sc.part_m, sc.part_s);
+  launch(race_kernel, dim3(B, CH), 256, 0, s, d, V, logits, tokens, q, T, seed, CH, sc.part_m, sc.part_i,
                                           sc.part_s, sc.race_k, sc.race_i, sc.req_R);
-  finalize_kernel<<<(B + 63) / 64, 64, 0, s>>>(d, B, tokens, T, CH, sc.part_m, sc.part_i, sc.part_s,
+  launch(finalize_kernel, (B + 63) / 64, 64, 0, s, d, B, tokens, T, CH, sc.part_m, sc.part_i, sc.part_s,
                                                sc.race_k, sc.race_i, sc.req_R, accept_len, out_tokens);
 }
 
@@ -304,13 +304,13 @@ void uniform_draws(uint64_t seed, uint32_t req, uint32_t tag, uint32_t row, uint
   if (n == 0) return;
   uint32_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  uniform_kernel<<<blocks, 256, 0, s>>>(seed, req, tag, row, n, out);
+  launch(uniform_kernel, blocks, 256, 0, s, seed, req, tag, row, n, out);
 }
 
 __global__ void clear_ints_kernel(int *p, int n) {
   for (int k = blockIdx.x * blockDim.x + threadIdx.x; k < n; k += gridDim.x * blockDim.x) p[k] = 0;
 }
 
-void clear_ints(int *p, int n, hipStream_t s) { clear_ints_kernel<<<1, 64, 0, s>>>(p, n); }
+void clear_ints(int *p, int n, hipStream_t s) { launch(clear_ints_kernel, 1, 64, 0, s, p, n); }
 
 }  // namespace wisp

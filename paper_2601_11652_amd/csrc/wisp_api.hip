@@ -149,31 +149,35 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
       p.g_lm = gemm_bf16_plan(p.M, p.V, p.d);
       p.g_lm.splits = 1;
       p.g_lm.kf_per_split = p.d / 16;
-      // split-KV work list: items of <= 48 query rows and a chunk of page pairs.  One wave
-      // per item and one 4-wave workgroup per CU are resident at a time, so the chunk is
-      // the shortest (of at most kAttnMaxChunkPages pages, whose block ids one wave keeps in
-      // a register) for which the items fill whole rounds of the device's wave slots: a
-      // round started by a few left-over workgroups would double the kernel's time.
+      // split-KV work list: items of <= 48 query rows and a run of page pairs.  One wave per
+      // item and one 4-wave workgroup per CU are resident at a time, so a round started by
+      // a few left-over workgroups would double the kernel's time; an item spans at most
+      // kAttnMaxChunkPages pages, whose block ids one wave keeps in a register.
       const int64_t slots = 4 * (int64_t)device_cus();
-      auto count_items = [&](int cp) {
+      // items of a group: its page pairs split into n equal parts (n = ceil(pairs / L)),
+      // L being the shortest item length (in pairs) whose items fill whole rounds of the
+      // device's wave slots; equal parts keep every wave's item close to L pairs, so no
+      // wave waits on a longer one
+      auto count_items = [&](int L) {
         int64_t n = 0;
         for (int i = 0; i < p.B; ++i) {
           const int rows = (d->gamma[i] + 1) * p.G;
           const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
-          const int64_t T = d->ctx_len[i] + d->gamma[i] + 1;
-          n += (int64_t)nrbg * p.nkv * ((T + 32 * cp - 1) / (32 * cp));
+          const int64_t pairs = (d->ctx_len[i] + d->gamma[i] + 1 + 31) / 32;
+          n += (int64_t)nrbg * p.nkv * ((pairs + L - 1) / L);
         }
         return n;
       };
-      const int cp_max = kAttnMaxChunkPages / 2;
+      const int L_max = kAttnMaxChunkPages / 2;
       int64_t rounds = 1;
-      const int64_t fewest = count_items(cp_max);
+      const int64_t fewest = count_items(L_max);
       while (rounds * slots < fewest) ++rounds;
-      int chunk_pairs = 2;
-      while (chunk_pairs < cp_max && count_items(chunk_pairs) > rounds * slots) ++chunk_pairs;
-      const int chunk = 32 * chunk_pairs;
+      int L = 2;
+      while (L < L_max && count_items(L) > rounds * slots) ++L;
       for (int i = 0; i < p.B; ++i) {
         const int T = d->ctx_len[i] + d->gamma[i] + 1;
+        const int pairs = (T + 31) / 32;
+        const int n = (pairs + L - 1) / L;
         const int rows = (d->gamma[i] + 1) * p.G;
         const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
         for (int h = 0; h < p.nkv; ++h)
@@ -183,12 +187,12 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
             gr.kvh = h;
             gr.rbg = g;
             gr.first_item = (int32_t)p.items.size();
-            for (int t0 = 0; t0 < T; t0 += chunk) {
+            for (int k = 0; k < n; ++k) {
               AttnItem it{};
               it.req = i;
               it.kvh_rbg = h | (g << 16);
-              it.t0 = t0;
-              it.t1 = std::min(T, t0 + chunk);
+              it.t0 = 32 * (int)((int64_t)k * pairs / n);
+              it.t1 = std::min(T, 32 * (int)((int64_t)(k + 1) * pairs / n));
               p.items.push_back(it);
             }
             gr.n_items = (int32_t)p.items.size() - gr.first_item;
@@ -263,15 +267,22 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
 }
 
 // ------------------------------------------------------------------------------------------
-// optional per-kernel-class timing (HIP events around each launch on the caller's stream)
+// optional per-kernel-class timing: while a class scope is open, every launch in it gets a
+// pair of HIP events stamped with that dispatch's own begin and end (launch_timing_events);
+// a class's time is the sum of its dispatches' durations, its launch count the number of
+// scopes, and its bytes / flops are those of the scope
 // ------------------------------------------------------------------------------------------
 struct ProfRec {
   int kind;
-  double bytes, flops;
+  int scopes;                 // 1 on a scope's first dispatch, else 0
+  double bytes, flops;        // the scope's figures, on its first dispatch
   hipEvent_t a, b;
 };
 struct ProfState {
   bool on = false;
+  int open_kind = -1;         // class of the open scope (-1: none)
+  bool open_first = false;    // no dispatch of the open scope recorded yet
+  double open_bytes = 0, open_flops = 0;
   std::vector<ProfRec> pending;
   std::vector<hipEvent_t> free_events;
   double ms[WISP_PROF_KINDS] = {}, bytes[WISP_PROF_KINDS] = {}, flops[WISP_PROF_KINDS] = {};
@@ -290,24 +301,16 @@ hipEvent_t prof_event() {
   return e;
 }
 
-struct ProfScope {   // records [begin, end) of one launch when profiling is on
-  int kind;
-  double bytes, flops;
-  hipStream_t s;
-  hipEvent_t a = nullptr;
-  ProfScope(int k, double by, double fl, hipStream_t st) : kind(k), bytes(by), flops(fl), s(st) {
+struct ProfScope {   // opens a timing scope of class `kind` over the launches it encloses
+  ProfScope(int kind, double bytes, double flops, hipStream_t) {
     if (g_prof.on) {
-      a = prof_event();
-      (void)hipEventRecord(a, s);
+      g_prof.open_kind = kind;
+      g_prof.open_first = true;
+      g_prof.open_bytes = bytes;
+      g_prof.open_flops = flops;
     }
   }
-  ~ProfScope() {
-    if (a) {
-      hipEvent_t b = prof_event();
-      (void)hipEventRecord(b, s);
-      g_prof.pending.push_back({kind, bytes, flops, a, b});
-    }
-  }
+  ~ProfScope() { g_prof.open_kind = -1; }
 };
 
 void prof_collect() {
@@ -318,12 +321,31 @@ void prof_collect() {
     g_prof.ms[r.kind] += ms;
     g_prof.bytes[r.kind] += r.bytes;
     g_prof.flops[r.kind] += r.flops;
-    g_prof.launches[r.kind] += 1;
+    g_prof.launches[r.kind] += r.scopes;
     g_prof.free_events.push_back(r.a);
     g_prof.free_events.push_back(r.b);
   }
   g_prof.pending.clear();
 }
+
+}  // namespace
+
+bool wisp::launch_timing_events(hipEvent_t *start, hipEvent_t *stop) {
+  if (!g_prof.on || g_prof.open_kind < 0) return false;
+  ProfRec r{g_prof.open_kind, 0, 0.0, 0.0, prof_event(), prof_event()};
+  if (g_prof.open_first) {
+    r.scopes = 1;
+    r.bytes = g_prof.open_bytes;
+    r.flops = g_prof.open_flops;
+    g_prof.open_first = false;
+  }
+  g_prof.pending.push_back(r);
+  *start = r.a;
+  *stop = r.b;
+  return true;
+}
+
+namespace {
 
 // pinned staging for the descriptor upload, reused once the previous copy has finished
 struct Staging {
