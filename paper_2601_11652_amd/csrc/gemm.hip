@@ -7,6 +7,8 @@
 // sum(gamma+1) rows) shapes are HBM-bound on the weight stream; K is split across
 // workgroups when there are too few output tiles to fill the 256 CUs, and the fp32
 // partial sums are added in a fixed order by the consuming epilogue kernel.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -172,10 +174,15 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
     return ld16_stream(W + (((int64_t)nb * KF + kq) * 64 + lane) * 8);
   };
   uint4 ring[R][NT];
+  // first R weight fragments; issued after the first activation chunk's loads, so that
+  // the chunk's LDS store (which waits for its loads, and memory counters complete in
+  // order) does not also wait for the weights' longer trip from HBM
+  auto ring_fill = [&]() {
 #pragma unroll
-  for (int r = 0; r < R; ++r)
+    for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, chunk_k(0) + r);
+      for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, chunk_k(0) + r);
+  };
 
   // Activations reach LDS through register sets.  AD = 2: two sets, chunk c is loaded into
   // set c % 2 two chunks before it is needed and written to LDS buffer c % 2 at the end of
@@ -202,7 +209,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
     }
   };
   // one chunk of R K steps from LDS buffer `buf`, refilling the ring from chunk ch + 1
-  auto chunk = [&](int buf, int ch) {
+  // `refill` is false for the last chunk: its refills would fetch fragments that are never
+  // used, and the workgroup could not finish before they had arrived
+  auto chunk = [&](int buf, int ch, auto refill) {
+    constexpr bool kRefill = decltype(refill)::value;
     const int kn = chunk_k(ch + 1);
     uint4 acur[MT], anext[MT];
 #pragma unroll
@@ -225,8 +235,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
         for (int j = 0; j < NT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(acur[i]), as_bf16x8(ring[r][j]),
                                                              acc[i][j], 0, 0, 0);
+      if constexpr (kRefill) {
 #pragma unroll
-      for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, kn + r);
+        for (int j = 0; j < NT; ++j) ring[r][j] = wload(j, kn + r);
+      }
       if (r + 1 < R) {
 #pragma unroll
         for (int i = 0; i < MT; ++i) acur[i] = anext[i];
@@ -237,32 +249,40 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
 
   if constexpr (AD == 2) {
     aload(0, 0);
+    ring_fill();
     astore(0, 0);
     __syncthreads();
     aload(1, 1);
     aload(0, 2);
-    for (int ch = 0; ch < nch; ch += 2) {   // straight-line body: every load unconditional
-      chunk(0, ch);
+    const std::true_type more;
+    for (int ch = 0; ch + 2 < nch; ch += 2) {   // straight-line body: every load unconditional
+      chunk(0, ch, more);
       astore(1, 1);       // chunk ch + 1
       __syncthreads();
       aload(1, ch + 3);
-      chunk(1, ch + 1);
+      chunk(1, ch + 1, more);
       astore(0, 0);       // chunk ch + 2
       __syncthreads();
       aload(0, ch + 4);
     }
+    chunk(0, nch - 2, more);   // the last pair (nch is even and >= 2)
+    astore(1, 1);
+    __syncthreads();
+    chunk(1, nch - 1, std::false_type{});
   } else {
     aload(0, 0);
+    ring_fill();
     astore(0, 0);
     __syncthreads();
     if (nch > 1) aload(0, 1);
-    for (int ch = 0; ch < nch; ++ch) {
+    for (int ch = 0; ch + 1 < nch; ++ch) {
       const int buf = ch & 1;
-      chunk(buf, ch);
-      if (ch + 1 < nch) astore(0, buf ^ 1);
+      chunk(buf, ch, std::true_type{});
+      astore(0, buf ^ 1);
       __syncthreads();
       if (ch + 2 < nch) aload(0, ch + 2);
     }
+    chunk((nch - 1) & 1, nch - 1, std::false_type{});
   }
 
   float *Cz = C + (int64_t)zs * M * ldc;
@@ -284,11 +304,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
 
 static constexpr int kKS = 4;
 static constexpr int kNarrowAD = 1;   // activation prefetch depth of the 32-column ring
+// From this many 32-row fragments on, the 32-column ring runs 8 waves per workgroup (two per
+// SIMD, each on half of the rows), so one wave's products issue while the other waits for
+// memory; below it the extra zero rows and doubled weight requests cost more than that buys
+static constexpr int kPairedWavesMinMT = 5;
 
 // Launch plan.  M <= 256 (the verification step's sum(gamma+1) rows for the batch sizes
 // served here): weight-ring kernels that hold all of A per workgroup; wide outputs use
 // 64-column wave tiles (one A fragment feeds two products), narrow ones 32-column tiles
-// with a deeper ring.  K is split until one workgroup per CU is in flight (one round).
+// with a deeper ring (8 waves per workgroup from kPairedWavesMinMT row fragments on).  K is
+// split until one workgroup per CU is in flight (one round).
 // Larger M: the LDS-tiled kernel.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
@@ -296,7 +321,7 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   const int KF = K / 16;
   int tiles, R;
   if (mf <= 8) {
-    c.kind = N >= 16384 ? 2 : 1;
+    c.kind = N >= 16384 ? 2 : (mf >= kPairedWavesMinMT ? 3 : 1);
     c.mt = mf;
     c.bm = 32 * mf;
     c.bn = c.kind == 2 ? 256 : 128;
@@ -320,6 +345,15 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   c.splits = (KF + kps - 1) / kps;
   c.kf_per_split = kps;
   return c;
+}
+
+// 32-column ring, 8 waves: two row halves of ceil(mt / 2) fragments each
+static void launch_ring_paired(int mt, dim3 grid, const uint16_t *A, const uint16_t *W, float *C, int M,
+                               int N, int K, int ldc, int kps, hipStream_t s) {
+  switch ((mt + 1) / 2) {
+    case 3: launch(gemm_ring_kernel<2, 4, 3, 1, 8, 2>, grid, 512, 0, s, A, W, C, M, N, K, ldc, kps); break;
+    case 4: launch(gemm_ring_kernel<2, 4, 4, 1, 8, 2>, grid, 512, 0, s, A, W, C, M, N, K, ldc, kps); break;
+  }
 }
 
 template <int NT, int R, int AD>
@@ -350,6 +384,8 @@ void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int
   dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, 1, 1);
   if (cfg.kind == 1)
     launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+  else if (cfg.kind == 3)
+    launch_ring_paired(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
   else
     launch_ring<2, 4, 2>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
 }

@@ -8,6 +8,9 @@
 * a batch of plain-decode requests only (no draft rows; the draft distributions may be
   NULL);
 * more than 256 rows (24 requests x 17 rows = 408), which takes the LDS-tiled GEMM path;
+* 129-256 rows, where the 32-column weight-ring GEMM runs 8 waves on two row halves: an
+  odd number of 32-row fragments (150 rows: one half carries a zero fragment) and an even
+  one (192 rows);
 * an out-of-range block id in the page table: the kernels clamp it, write nothing through
   it, and wisp_check reports a device input error.
 """
@@ -124,6 +127,12 @@ def test_more_than_256_rows_takes_the_tiled_gemm():
     B = 24
     ctx = [int(c) for c in np.random.default_rng(5).integers(0, 96, size=B)]
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs, 6e-2)
+
+
+@pytest.mark.parametrize("B,gamma", [(10, 14), (12, 15)], ids=["150rows", "192rows"])
+def test_paired_wave_ring_gemm_rows(B, gamma):
+    ctx = [int(c) for c in np.random.default_rng(B).integers(0, 80, size=B)]
+    _run_case(MINI_BF16, ctx, [gamma] * B, _bf16_abs, 6e-2)
 
 
 def test_out_of_range_block_id_is_reported():
