@@ -12,9 +12,11 @@ same batch is verified W + K times, each time with its own acceptance seed.  Met
 committed (accepted + extra) tokens per second, sum(L_i + 1) averaged over the K timed
 steps' draws / step time, with the step latency alongside.
 
-Prints ONE JSON line.  Also reports the dominant kernel class against its roofline
-(algorithmic bytes per launch over the HIP-event-timed average launch) and the CPU
-oracle timed on a bounded sample of the same workload.
+Prints ONE JSON line.  Also reports the median and p90 step time, the whole step against
+its roofline lower bound (each kernel class's algorithmic bytes or flops at the HBM or
+MFMA peak), the dominant kernel class against its roofline (algorithmic bytes per launch
+over the HIP-event-timed average launch) and the CPU oracle timed on a bounded sample of
+the same workload.  `--sweep 1,2,4,...` prints the batch-size curve instead.
 """
 from __future__ import annotations
 
@@ -127,13 +129,125 @@ def cpu_baseline(mix, sample_req: int):
                        f"{s.n_layers} layers plus acceptance, {committed} committed tokens in {dt:.2f} s")}
 
 
+def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = True):
+    """Fill the KV pool and draft fixture of `mix`, then time `steps` verification steps
+    (after `warmup` untimed ones) back to back on the current stream.  Returns the step
+    figures and, with `profile`, the per-kernel-class durations."""
+    import ctypes as C
+    import numpy as np
+    import torch
+    s = mix.shape
+    pt_np, n_blocks = wi.page_table(mix)
+    dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
+    kv = W.KVPool.zeros(s.n_layers, n_blocks, s.n_kv_heads, s.head_dim, dt)
+    t0 = time.time()
+    wi.fill_kv_pool(kv.k, kv.v, mix, pt_np)
+    torch.cuda.synchronize()
+    log(f"B = {mix.B}: KV pool {kv.k.numel() * 2 * kv.k.element_size() / 2**30:.2f} GiB filled in {time.time() - t0:.1f} s")
+    pt = torch.as_tensor(pt_np, device="cuda")
+    roots = wi.root_tokens(mix)
+    tokens, q = gpu_draft_fixture(W, gm, kv, mix, pt, roots)
+
+    desc = W.BatchDesc(mix.ctx_len, mix.gamma, pt, 1.0, mix.req_id)
+    ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
+    M = mix.M
+    # every timed step draws its own acceptance randomness (seed + step) into its own row of
+    # accepted lengths, so the committed-token count is a mean over the K steps' draws
+    accs = torch.empty((warmup + steps, mix.B), dtype=torch.int32, device="cuda")
+    out = torch.empty(M, dtype=torch.int32, device="cuda")
+    logits = torch.empty(M, s.vocab, dtype=torch.float32, device="cuda")
+    seed = wi.verify_seed(mix)
+
+    def step(i=0):
+        W.wisp_verify(gm.c, kv, desc, tokens, q, seed + i, accs[i], out, logits, ws)
+
+    for i in range(warmup):
+        step(i)
+    W.wisp_check(ws)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for k, i in enumerate(range(warmup, warmup + steps)):
+        step(i)
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev[0].elapsed_time(ev[-1]) / steps
+    per_step = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)])
+    log(f"B = {mix.B}: {steps} steps: {ms_step:.3f} ms/step (events), {wall / steps * 1e3:.3f} ms/step (wall)")
+    L = accs[warmup:].cpu().numpy().astype(np.int64)
+    committed = float((L + 1).sum()) / steps
+    res = {"ms_per_step": ms_step, "ms_p50": float(np.median(per_step)), "ms_p90": float(np.percentile(per_step, 90)),
+           "committed": committed, "accepted": float(L.sum()) / steps, "M": M}
+
+    classes = {}
+    if profile:
+        # per-kernel-class durations: HIP events stamped by each dispatch on the library's stream
+        prof_steps = max(3, min(10, steps))
+        W.lib.wisp_profile_enable(1)
+        W.lib.wisp_profile_reset()
+        for _ in range(prof_steps):
+            step()
+        torch.cuda.synchronize()
+        for kind, name in KERNEL_CLASSES:
+            ms, n, by, fl = C.c_double(), C.c_int64(), C.c_double(), C.c_double()
+            W.lib.wisp_profile_read(kind, C.byref(ms), C.byref(n), C.byref(by), C.byref(fl))
+            if n.value:
+                classes[name] = {"ms_per_step": ms.value / prof_steps, "launches_per_step": n.value / prof_steps,
+                                 "avg_launch_us": ms.value / n.value * 1e3, "bytes_per_launch": by.value / n.value,
+                                 "flops_per_launch": fl.value / n.value,
+                                 "achieved_GBs": by.value / ms.value / 1e6 if ms.value else 0.0,
+                                 "achieved_TFLOPs": fl.value / ms.value / 1e9 if ms.value else 0.0}
+        W.lib.wisp_profile_enable(0)
+    res["classes"] = classes
+    del kv, ws, logits, q
+    return res
+
+
+def step_lower_bound(classes: dict) -> dict:
+    """Roofline lower bound of a whole step: each kernel class's algorithmic bytes at the HBM
+    peak or its flops at the bf16 MFMA peak, whichever is longer, summed over the classes."""
+    lb = 0.0
+    by = 0.0
+    for c in classes.values():
+        b = c["bytes_per_launch"] * c["launches_per_step"]
+        f = c["flops_per_launch"] * c["launches_per_step"]
+        by += b
+        lb += max(b / (HBM_PEAK_GBS * 1e9), f / (BF16_PEAK_TFLOPS * 1e12))
+    return {"lower_bound_ms": lb * 1e3, "bytes_per_step": by}
+
+
+def sweep(args, W, wi, gm):
+    """The batch-size curve: the same request distributions at B = 1 .. 256, one JSON line
+    per batch size (tokens/s and step latency), written to --sweep-out as well."""
+    rows = []
+    for B in [int(b) for b in args.sweep.split(",")]:
+        mix = wi.make_mix(args.config, B=B)
+        r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True)
+        lb = step_lower_bound(r["classes"])
+        row = {"B": B, "rows": r["M"], "sum_ctx": int(mix.ctx_len.sum()), "ms_per_step": r["ms_per_step"],
+               "ms_p50": r["ms_p50"], "ms_p90": r["ms_p90"], "committed_tokens_per_step": r["committed"],
+               "tokens_per_s": r["committed"] / (r["ms_per_step"] / 1e3),
+               "accepted_drafts_per_s": r["accepted"] / (r["ms_per_step"] / 1e3),
+               "step_lower_bound_ms": lb["lower_bound_ms"], "step_frac": lb["lower_bound_ms"] / r["ms_per_step"]}
+        rows.append(row)
+        print(json.dumps(row), flush=True)
+    if args.sweep_out:
+        with open(args.sweep_out, "w") as f:
+            json.dump({"config": args.config, "steps": args.steps, "warmup": args.warmup, "rows": rows}, f, indent=1)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="8b_b32")
-    ap.add_argument("--B", type=int, default=None, help="override the batch size (sweeps)")
+    ap.add_argument("--B", type=int, default=None, help="override the batch size")
+    ap.add_argument("--sweep", default=None, help="comma-separated batch sizes: print the batch-size curve instead")
+    ap.add_argument("--sweep-out", default=None, help="also write the curve to this JSON file")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM counter scaling)")
@@ -155,69 +269,16 @@ def main():
     t0 = time.time()
     gm = W.GpuModel(s, lambda l: wi.layer_weights(s, l, mix.seed, "cuda"), wi.global_weights(s, mix.seed, "cuda"))
     log(f"weights generated and packed in {time.time() - t0:.1f} s")
-    pt_np, n_blocks = wi.page_table(mix)
-    dt = torch.bfloat16 if s.dtype == "bf16" else torch.float32
-    kv = W.KVPool.zeros(s.n_layers, n_blocks, s.n_kv_heads, s.head_dim, dt)
-    t0 = time.time()
-    wi.fill_kv_pool(kv.k, kv.v, mix, pt_np)
-    torch.cuda.synchronize()
-    log(f"KV pool {kv.k.numel() * 2 * kv.k.element_size() / 2**30:.2f} GiB filled in {time.time() - t0:.1f} s")
-    pt = torch.as_tensor(pt_np, device="cuda")
-    roots = wi.root_tokens(mix)
-    tokens, q = gpu_draft_fixture(W, gm, kv, mix, pt, roots)
-    log("draft fixture ready")
+    if args.sweep:
+        sweep(args, W, wi, gm)
+        return
 
-    desc = W.BatchDesc(mix.ctx_len, mix.gamma, pt, 1.0, mix.req_id)
-    ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
-    M = mix.M
-    # every timed step draws its own acceptance randomness (seed + step) into its own row of
-    # accepted lengths, so the committed-token count is a mean over the K steps' draws
-    accs = torch.empty((args.warmup + args.steps, mix.B), dtype=torch.int32, device="cuda")
-    out = torch.empty(M, dtype=torch.int32, device="cuda")
-    logits = torch.empty(M, s.vocab, dtype=torch.float32, device="cuda")
-    seed = wi.verify_seed(mix)
-
-    def step(i=0):
-        W.wisp_verify(gm.c, kv, desc, tokens, q, seed + i, accs[i], out, logits, ws)
-
-    for i in range(args.warmup):
-        step(i)
-    W.wisp_check(ws)
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    e0.record(stream)
-    for i in range(args.warmup, args.warmup + args.steps):
-        step(i)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = e0.elapsed_time(e1) / args.steps
-    log(f"{args.steps} steps: {ms_step:.3f} ms/step (events), {wall / args.steps * 1e3:.3f} ms/step (wall)")
-    L = accs[args.warmup:].cpu().numpy().astype(np.int64)
-    committed = float((L + 1).sum()) / args.steps
+    r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True)
+    ms_step = r["ms_per_step"]
+    committed = r["committed"]
     value = committed / (ms_step / 1e3)
-
-    # per-kernel-class durations: HIP events around each launch on the library's stream
-    prof_steps = max(3, min(10, args.steps))
-    W.lib.wisp_profile_enable(1)
-    W.lib.wisp_profile_reset()
-    for _ in range(prof_steps):
-        step()
-    torch.cuda.synchronize()
-    classes = {}
-    import ctypes as C
-    for kind, name in KERNEL_CLASSES:
-        ms, n, by, fl = C.c_double(), C.c_int64(), C.c_double(), C.c_double()
-        W.lib.wisp_profile_read(kind, C.byref(ms), C.byref(n), C.byref(by), C.byref(fl))
-        if n.value:
-            classes[name] = {"ms_per_step": ms.value / prof_steps, "launches_per_step": n.value / prof_steps,
-                             "avg_launch_us": ms.value / n.value * 1e3, "bytes_per_launch": by.value / n.value,
-                             "flops_per_launch": fl.value / n.value,
-                             "achieved_GBs": by.value / ms.value / 1e6 if ms.value else 0.0,
-                             "achieved_TFLOPs": fl.value / ms.value / 1e9 if ms.value else 0.0}
-    W.lib.wisp_profile_enable(0)
+    classes = r["classes"]
+    M = mix.M
     dom = max((k for k in classes if classes[k]["bytes_per_launch"] > 0), key=lambda k: classes[k]["ms_per_step"])
     c = classes[dom]
     mfma_bound = dom.startswith("gemm") and M >= 630
@@ -227,8 +288,8 @@ def main():
         roof = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["kernel"] = KERNEL_NAMES[dom]
-    tr = traffic_from_counters(f"{dom}_{args.config}")
-    roof["traffic"] = tr
+    roof["traffic"] = traffic_from_counters(f"{dom}_{args.config}")
+    lb = step_lower_bound(classes)
 
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -253,9 +314,13 @@ def main():
         "config": {"workload": f"{args.config}: {s.name} verification step", "B": mix.B, "rows": M,
                    "sum_ctx": int(mix.ctx_len.sum()), "sum_gamma": int(mix.gamma.sum()), "page": 16,
                    "layers": s.n_layers, "vocab": s.vocab},
-        "accepted_drafts_per_s": float(L.sum()) / args.steps / (ms_step / 1e3),
-        "acceptance_rate": float(L.sum()) / args.steps / max(1, int(mix.gamma.sum())),
+        "ms_p50": r["ms_p50"],
+        "ms_p90": r["ms_p90"],
+        "accepted_drafts_per_s": r["accepted"] / (ms_step / 1e3),
+        "acceptance_rate": r["accepted"] / max(1, int(mix.gamma.sum())),
         "committed_tokens_per_step": committed,
+        "step_roofline": {"lower_bound_ms": lb["lower_bound_ms"], "frac": lb["lower_bound_ms"] / ms_step,
+                          "bytes_per_step": lb["bytes_per_step"]},
         "roofline": roof,
         "kernels": classes,
     }

@@ -308,32 +308,42 @@ static constexpr int kNarrowAD = 1;   // activation prefetch depth of the 32-col
 // SIMD, each on half of the rows), so one wave's products issue while the other waits for
 // memory; below it the extra zero rows and doubled weight requests cost more than that buys
 static constexpr int kPairedWavesMinMT = 5;
+// Up to this many row blocks of <= 256 rows the weight-ring kernels serve any M: each block
+// re-streams the weights, mostly from L2 / MALL while the blocks of a tile run together
+static constexpr int kRingMaxRowBlocks = 8;
 
-// Launch plan.  M <= 256 (the verification step's sum(gamma+1) rows for the batch sizes
-// served here): weight-ring kernels that hold all of A per workgroup; wide outputs use
-// 64-column wave tiles (one A fragment feeds two products), narrow ones 32-column tiles
-// with a deeper ring (8 waves per workgroup from kPairedWavesMinMT row fragments on).  K is
-// split until one workgroup per CU is in flight (one round).
-// Larger M: the LDS-tiled kernel.
+// Launch plan.  Weight-ring kernels whose workgroups hold all rows of a row block of at most
+// 256 rows (one block for the verification step's sum(gamma+1) rows at moderate batch
+// sizes, up to kRingMaxRowBlocks blocks beyond); wide outputs use 64-column wave tiles (one
+// A fragment feeds two products), narrow ones 32-column tiles with a deeper ring (8 waves
+// per workgroup from kPairedWavesMinMT row fragments on).  K is split until one workgroup
+// per CU is in flight (one round).  Beyond 2048 rows: the LDS-tiled kernel.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
   const int KF = K / 16;
   int tiles, R;
-  if (mf <= 8) {
-    c.kind = N >= 16384 ? 2 : (mf >= kPairedWavesMinMT ? 3 : 1);
-    c.mt = mf;
-    c.bm = 32 * mf;
+  if (mf <= kRingMaxRowBlocks * 8) {
+    // rows in rb blocks of at most 8 fragments, balanced; each block is one grid row of
+    // workgroups that stream the same weights (the grid width is a multiple of 8 for every
+    // projection here, so a tile's row blocks share an XCD and its L2)
+    c.rb = (mf + 7) / 8;
+    int mt = (mf + c.rb - 1) / c.rb;
+    c.kind = N >= 16384 ? 2 : (mt >= kPairedWavesMinMT ? 3 : 1);
+    if (c.kind == 3 && c.rb > 1) mt += mt & 1;   // paired halves: a block is 2 * ceil(mt / 2) fragments
+    c.mt = mt;
+    c.bm = 32 * mt;
     c.bn = c.kind == 2 ? 256 : 128;
     R = c.kind == 2 ? 4 : 8;
-    tiles = (N + c.bn - 1) / c.bn;
+    tiles = ((N + c.bn - 1) / c.bn) * c.rb;
   } else {
     c.kind = 0;
     c.mt = 0;
+    c.rb = (M + 255) / 256;
     c.bm = 256;
     c.bn = 128;
     R = kKS;
-    tiles = ((N + c.bn - 1) / c.bn) * ((M + c.bm - 1) / c.bm);
+    tiles = ((N + c.bn - 1) / c.bn) * c.rb;
   }
   // workgroups resident at once: the ring kernels hold one workgroup per CU (LDS and
   // registers), so more than one round of 256 would leave a partial second round
@@ -381,7 +391,7 @@ void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int
     launch(gemm_bf16_kernel<2, 2, 4, 2, kKS>, grid, 256, 0, s, A, W, C, M, N, K, ldc, cfg.kf_per_split);
     return;
   }
-  dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, 1, 1);
+  dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, cfg.rb, 1);
   if (cfg.kind == 1)
     launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
   else if (cfg.kind == 3)
