@@ -45,6 +45,7 @@ typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
 
 #define WISP_PAGE 16        /* tokens per KV page                                            */
 #define WISP_GAMMA_MAX 16   /* most draft tokens per request                                 */
+#define WISP_PREFILL_MAX 32768 /* most uncached prompt tokens per request and call (prefill_len) */
 
 /*
  * Decoder-only transformer (RMSNorm, rotary embedding with rotate-half pairing,
@@ -101,6 +102,14 @@ typedef struct {
  * ctx_len[i] .. ctx_len[i] + gamma[i], where root is the last committed token
  * (the previous round's extra token), whose KV is not cached yet.  Row j's logits
  * score draft y_{j+1}; row gamma[i] is the bonus position.
+ *
+ * First-time (cold-start) verification and chunked prefill (Sec. 4.4's two verification
+ * types): prefill_len[i] > 0 adds that many uncached prompt tokens in front of the root,
+ * so the request forwards prefill_len[i] + gamma[i] + 1 rows [p_0 .. p_{P-1}, root,
+ * y_1 .. y_gamma] at positions ctx_len[i] ..; root is then the prompt's last token.  Their
+ * K/V are appended and they take part in the causal attention, but only the gamma[i] + 1
+ * verification rows produce logits and enter the acceptance.  A cold start has
+ * ctx_len[i] = 0; a later chunk of a long prompt has the earlier chunks cached.
  */
 typedef struct {
   int32_t B;
@@ -110,6 +119,8 @@ typedef struct {
   const int32_t *kv_page_table;  /* DEVICE [B][pt_stride] block ids                         */
   int32_t pt_stride;             /* pages per request in the table                         */
   float temperature;             /* target temperature: > 0 sampled, 0 greedy              */
+  const int32_t *prefill_len;    /* HOST [B]  0..WISP_PREFILL_MAX uncached prompt tokens
+                                    before the root; NULL = none                            */
 } wisp_batch_desc;
 
 /* Bytes of DEVICE workspace wisp_verify needs for this model and batch (0 on error). */
@@ -130,7 +141,8 @@ wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t c
 
 /*
  * The verification step (Sec. 4.5): forward + acceptance, returns L and the extra token.
- *   tokens        DEVICE int32 [M], M = sum(gamma+1): per request root, y_1..y_gamma
+ *   tokens        DEVICE int32 [sum(prefill_len+gamma+1)]: per request the prompt tokens
+ *                 (prefill_len of them), root, y_1..y_gamma; M below = sum(gamma+1)
  *   draft_probs   DEVICE fp32 [sum gamma][vocab]: q_j rows, request-major (finite, >= 0)
  *   rng_seed      keys every random draw (Philox4x32-10, Salmon et al. SC'11): the
  *                 acceptance draw of draft j uses counter (0, j, req_id, 1), word 0; the
@@ -139,11 +151,12 @@ wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t c
  *                 (2 * (w >> 9) + 1) * 2^-24 in (0, 1).  Vary the seed between rounds.
  *   accept_len    DEVICE int32 [B]: L_i = R_i - 1 (Eq. (2))
  *   out_tokens    DEVICE int32 [M]: request i's slots hold y_1..y_L, the extra token, then -1
- *   target_logits DEVICE fp32 [M][vocab]: the target's logits of every row (required)
+ *   target_logits DEVICE fp32 [M][vocab]: the target's logits of every verification row
+ *                 (root .. y_gamma of each request; prompt rows produce none) (required)
  *   workspace     DEVICE scratch of >= wisp_workspace_size() bytes
- * KV: K/V of all gamma+1 new positions are written in place (rejected drafts
- * included); the valid prefix afterwards is ctx_len + 1 + L and later calls overwrite
- * the stale slots (rollback by length).  Repeating a call with the same inputs gives
+ * KV: K/V of all prefill_len+gamma+1 new positions are written in place (rejected
+ * drafts included); the valid prefix afterwards is ctx_len + prefill_len + 1 + L and
+ * later calls overwrite the stale slots (rollback by length).  Repeating a call with the same inputs gives
  * the same outputs.  Extra tokens are drawn by an exponential race (Gumbel-max):
  * argmax_k [score_k - ln(-ln u_k)], ties to the smallest k, score = ln(residual) after
  * a rejection (or z = logits/T when the residual is empty), z after full acceptance.

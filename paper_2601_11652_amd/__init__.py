@@ -64,7 +64,7 @@ class wisp_kv(C.Structure):
 class wisp_batch_desc(C.Structure):
     _fields_ = [("B", C.c_int32), ("ctx_len", C.POINTER(C.c_int32)), ("gamma", C.POINTER(C.c_int32)),
                 ("req_id", C.POINTER(C.c_uint32)), ("kv_page_table", _VP), ("pt_stride", C.c_int32),
-                ("temperature", C.c_float)]
+                ("temperature", C.c_float), ("prefill_len", C.POINTER(C.c_int32))]
 
 
 _lib = None
@@ -144,10 +144,12 @@ def _stream(stream) -> int | None:
 class BatchDesc:
     """Owns the host arrays behind a wisp_batch_desc."""
 
-    def __init__(self, ctx_len, gamma, page_table=None, temperature: float = 1.0, req_id=None):
+    def __init__(self, ctx_len, gamma, page_table=None, temperature: float = 1.0, req_id=None,
+                 prefill_len=None):
         self.ctx_len = np.ascontiguousarray(ctx_len, dtype=np.int32)
         self.gamma = np.ascontiguousarray(gamma, dtype=np.int32)
         self.req_id = None if req_id is None else np.ascontiguousarray(req_id, dtype=np.uint32)
+        self.prefill_len = None if prefill_len is None else np.ascontiguousarray(prefill_len, dtype=np.int32)
         self.page_table = page_table          # torch int32 [B][stride] on the device
         B = self.ctx_len.shape[0]
         self.c = wisp_batch_desc()
@@ -161,6 +163,8 @@ class BatchDesc:
             self.c.kv_page_table = page_table.data_ptr()
             self.c.pt_stride = page_table.shape[1]
         self.c.temperature = float(temperature)
+        self.c.prefill_len = (self.prefill_len.ctypes.data_as(C.POINTER(C.c_int32))
+                              if self.prefill_len is not None else None)
 
     @property
     def B(self):
@@ -168,7 +172,14 @@ class BatchDesc:
 
     @property
     def M(self):
+        """Verification rows (logits rows): sum(gamma + 1)."""
         return int((self.gamma.astype(np.int64) + 1).sum())
+
+    @property
+    def rows(self):
+        """Forwarded rows (token count): sum(prefill_len + gamma + 1)."""
+        pre = 0 if self.prefill_len is None else int(self.prefill_len.astype(np.int64).sum())
+        return self.M + pre
 
     @property
     def S(self):

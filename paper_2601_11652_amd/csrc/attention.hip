@@ -42,10 +42,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
   item.t1 = __builtin_amdgcn_readfirstlane(items[it].t1);
   const int i = item.req, kvh = item.kvh_rbg & 0xFFFF, rbg = item.kvh_rbg >> 16;
   const int G = nq / nkv;
-  const int gam = __builtin_amdgcn_readfirstlane(d.gamma[i]);
+  const int nrw = __builtin_amdgcn_readfirstlane(d.nrow[i]);
   const int ctx = __builtin_amdgcn_readfirstlane(d.ctx[i]);
   const int off = __builtin_amdgcn_readfirstlane(d.off[i]);
-  const int rows = (gam + 1) * G;
+  const int rows = nrw * G;
   const int lr0 = rbg * (16 * RB);
   // row blocks this wave carries: at least one (an item always has rows), written so the
   // compiler can see it and never skips a pair's products (a skipped product would leave
@@ -237,7 +237,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
   if (gi >= n_groups) return;
   const AttnGroup g = groups[gi];
   const int G = nq / nkv;
-  const int rows = (d.gamma[g.req] + 1) * G;
+  const int rows = d.nrow[g.req] * G;
   const int lr0 = g.rbg * kAttnRowsPerItem;
   const int nr = min(kAttnRowsPerItem, rows - lr0);
   const int u = (int)(u_all % UNITS);
@@ -345,10 +345,10 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(StepDesc d, const float *
   __shared__ float sh[4];
   const int i = blockIdx.x / nq, hq = blockIdx.x % nq;
   const int kvh = hq / (nq / nkv);
-  const int gam = d.gamma[i], ctx = d.ctx[i], off = d.off[i];
+  const int nrw = d.nrow[i], ctx = d.ctx[i], off = d.off[i];
   const int32_t *pt = d.page_table + (int64_t)i * d.pt_stride;
   const int page_elems = kPage * hd;
-  for (int j = 0; j <= gam; ++j) {
+  for (int j = 0; j < nrw; ++j) {
     const int64_t r = off + j;
     const float *qr = q + (r * nq + hq) * hd;
     const int T = ctx + j + 1;

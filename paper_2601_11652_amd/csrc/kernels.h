@@ -47,6 +47,7 @@ struct StepDesc {         // device arrays carved from the workspace
   const uint32_t *req_id; // [B]
   const int32_t *row_req; // [M]
   const int32_t *row_pos; // [M]
+  const int32_t *nrow;    // [B] rows forwarded per request (prompt tokens, root, drafts)
   const int32_t *page_table;
   int pt_stride;
   int n_blocks;
@@ -59,9 +60,13 @@ template <typename T>
 void embed_norm(const StepDesc &d, const T *embed, const T *gain, const int32_t *tokens, float *h,
                 T *xn, bool packed, int M, int dm, int V, float eps, hipStream_t s);
 
+// h += sum of the split partials, xn = RMSNorm(h) * gain; rows (optional) maps each of the
+// n_out output rows to its source row (NULL: n_out = M, identity)
 template <typename T>
 void resid_norm(const float *part, int splits, float *h, const T *gain, T *xn, bool packed, int M,
-                int dm, float eps, hipStream_t s);
+                int dm, float eps, hipStream_t s, const int32_t *rows = nullptr, int n_out = -1);
+// dst[i] = src[idx[i]], i < n
+void gather_ints(const int32_t *src, const int32_t *idx, int n, int32_t *dst, hipStream_t s);
 
 template <typename T>
 void qkv_rope_append(const StepDesc &d, const float *part, int splits, const float *cs, T *q,

@@ -148,9 +148,11 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(const float *__restric
                                                           float *__restrict__ h,
                                                           const T *__restrict__ gain,
                                                           T *__restrict__ xn, bool packed, int M,
-                                                          int dm, float eps) {
+                                                          int dm, float eps,
+                                                          const int32_t *__restrict__ rows) {
   __shared__ float sh[16];
-  const int r = blockIdx.x;
+  const int ro = blockIdx.x;                 // output row
+  const int r = rows ? rows[ro] : ro;        // source row
   const int c = threadIdx.x * 8;
   const bool on = c < dm;
   float v[8];
@@ -175,14 +177,26 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(const float *__restric
   const float inv = 1.0f / sqrtf(ss / (float)dm + eps);
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] = v[e] * inv * Act<T>::load(gain, c + e);
-  store8<T>(xn, packed, r, c, dm, v);
+  store8<T>(xn, packed, ro, c, dm, v);
 }
 
 template <typename T>
 void resid_norm(const float *part, int splits, float *h, const T *gain, T *xn, bool packed, int M,
-                int dm, float eps, hipStream_t s) {
+                int dm, float eps, hipStream_t s, const int32_t *rows, int n_out) {
   const int threads = ((dm / 8 + 63) / 64) * 64;   // dm <= 8192
-  launch(resid_norm_kernel<T>, M, threads, 0, s, part, splits, h, gain, xn, packed, M, dm, eps);
+  const int n = rows ? n_out : M;
+  if (n <= 0) return;
+  launch(resid_norm_kernel<T>, n, threads, 0, s, part, splits, h, gain, xn, packed, M, dm, eps, rows);
+}
+
+__global__ void gather_ints_kernel(const int32_t *__restrict__ src, const int32_t *__restrict__ idx, int n,
+                                   int32_t *__restrict__ dst) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[idx[i]];
+}
+
+void gather_ints(const int32_t *src, const int32_t *idx, int n, int32_t *dst, hipStream_t s) {
+  if (n > 0) launch(gather_ints_kernel, (n + 255) / 256, 256, 0, s, src, idx, n, dst);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -315,9 +329,9 @@ template void embed_norm<uint16_t>(const StepDesc &, const uint16_t *, const uin
                                    const int32_t *, float *, uint16_t *, bool, int, int, int, float,
                                    hipStream_t);
 template void resid_norm<float>(const float *, int, float *, const float *, float *, bool, int, int,
-                                float, hipStream_t);
+                                float, hipStream_t, const int32_t *, int);
 template void resid_norm<uint16_t>(const float *, int, float *, const uint16_t *, uint16_t *, bool,
-                                   int, int, float, hipStream_t);
+                                   int, int, float, hipStream_t, const int32_t *, int);
 template void qkv_rope_append<float>(const StepDesc &, const float *, int, const float *, float *,
                                      float *, float *, int, int, int, int, hipStream_t);
 template void qkv_rope_append<uint16_t>(const StepDesc &, const float *, int, const float *,

@@ -39,6 +39,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // ------------------------------------------------------------------------------------------
 struct Plan {
   int B = 0, M = 0, Mp = 0, S = 0;   // requests, rows, rows padded to 32, total drafts
+  int Mv = 0;                        // verification rows (root and drafts): logits rows
+  bool prefill = false;              // some request forwards prompt rows before its root
   int d = 0, nq = 0, nkv = 0, hd = 0, F = 0, V = 0, qdim = 0, kvdim = 0, qkvN = 0, G = 0;
   bool bf16 = false;
   int max_tokens = 0;
@@ -48,11 +50,11 @@ struct Plan {
   std::vector<int32_t> host;         // descriptor block uploaded to the device
   // int32 offsets inside the descriptor block
   size_t i_off = 0, i_doff = 0, i_gamma = 0, i_ctx = 0, i_req = 0, i_row_req = 0, i_row_pos = 0,
-         i_items = 0, i_groups = 0;
+         i_items = 0, i_groups = 0, i_voff = 0, i_nrow = 0, i_vrow = 0;
   // byte offsets inside the workspace
   size_t w_err = 0, w_desc = 0, w_rope = 0, w_h = 0, w_xn = 0, w_ao = 0, w_af = 0, w_q = 0,
          w_part = 0, w_attn_o = 0, w_attn_ml = 0, w_sm = 0, w_si = 0, w_ss = 0, w_rk = 0, w_ri = 0,
-         w_rR = 0, total = 0;
+         w_rR = 0, w_vtok = 0, total = 0;
 };
 
 
@@ -94,9 +96,14 @@ wisp_status check_desc(const wisp_batch_desc *d, bool need_pages) {
     if (d->gamma[i] < 0 || d->gamma[i] > WISP_GAMMA_MAX)
       return fail(WISP_E_INVALID, "gamma[%d] = %d outside 0..%d", i, d->gamma[i], WISP_GAMMA_MAX);
     if (d->ctx_len[i] < 0) return fail(WISP_E_INVALID, "ctx_len[%d] < 0", i);
-    if (need_pages && (int64_t)d->pt_stride * WISP_PAGE < (int64_t)d->ctx_len[i] + d->gamma[i] + 1)
-      return fail(WISP_E_CAPACITY, "request %d needs %d tokens but the page table holds %d", i,
-                  d->ctx_len[i] + d->gamma[i] + 1, d->pt_stride * WISP_PAGE);
+    const int pre = d->prefill_len ? d->prefill_len[i] : 0;
+    if (pre < 0 || pre > WISP_PREFILL_MAX)
+      return fail(WISP_E_INVALID, "prefill_len[%d] = %d outside 0..%d", i, pre, WISP_PREFILL_MAX);
+    const int64_t need = (int64_t)d->ctx_len[i] + pre + d->gamma[i] + 1;
+    if (need > INT32_MAX / 2) return fail(WISP_E_INVALID, "request %d: ctx_len too large", i);
+    if (need_pages && (int64_t)d->pt_stride * WISP_PAGE < need)
+      return fail(WISP_E_CAPACITY, "request %d needs %lld tokens but the page table holds %d", i,
+                  (long long)need, d->pt_stride * WISP_PAGE);
   }
   if (need_pages && !d->kv_page_table) return fail(WISP_E_INVALID, "kv_page_table is NULL");
   return WISP_OK;
@@ -120,12 +127,19 @@ int device_cus() {
 void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward, int vocab = 0) {
   p.B = d->B;
   p.V = forward ? m->vocab : vocab;
-  std::vector<int> off(p.B + 1, 0), doff(p.B + 1, 0);
+  // rows of request i: prefill_len prompt rows (forward only), root, gamma drafts; the
+  // verification rows (root .. y_gamma) are the last gamma + 1 and alone produce logits
+  std::vector<int> off(p.B + 1, 0), doff(p.B + 1, 0), voff(p.B + 1, 0), nrow(p.B, 0);
   for (int i = 0; i < p.B; ++i) {
-    off[i + 1] = off[i] + d->gamma[i] + 1;
+    const int pre = (forward && d->prefill_len) ? d->prefill_len[i] : 0;
+    nrow[i] = pre + d->gamma[i] + 1;
+    off[i + 1] = off[i] + nrow[i];
+    voff[i + 1] = voff[i] + d->gamma[i] + 1;
     doff[i + 1] = doff[i] + d->gamma[i];
+    if (pre > 0) p.prefill = true;
   }
   p.M = off[p.B];
+  p.Mv = voff[p.B];
   p.S = doff[p.B];
   p.Mp = (p.M + 31) / 32 * 32;
   if (forward) {
@@ -140,13 +154,13 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
     p.kvdim = p.nkv * p.hd;
     p.qkvN = p.qdim + 2 * p.kvdim;
     p.bf16 = m->dtype == WISP_BF16;
-    for (int i = 0; i < p.B; ++i) p.max_tokens = std::max(p.max_tokens, d->ctx_len[i] + d->gamma[i] + 1);
+    for (int i = 0; i < p.B; ++i) p.max_tokens = std::max(p.max_tokens, d->ctx_len[i] + nrow[i]);
     if (p.bf16) {
       p.g_qkv = gemm_bf16_plan(p.M, p.qkvN, p.d);
       p.g_o = gemm_bf16_plan(p.M, p.d, p.qdim);
       p.g_gu = gemm_bf16_plan(p.M, 2 * p.F, p.d);
       p.g_down = gemm_bf16_plan(p.M, p.d, p.F);
-      p.g_lm = gemm_bf16_plan(p.M, p.V, p.d);
+      p.g_lm = gemm_bf16_plan(p.Mv, p.V, p.d);
       p.g_lm.splits = 1;
       p.g_lm.kf_per_split = p.d / 16;
       // split-KV work list: items of <= 48 query rows and a run of page pairs.  One wave per
@@ -158,13 +172,20 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
       // L being the shortest item length (in pairs) whose items fill whole rounds of the
       // device's wave slots; equal parts keep every wave's item close to L pairs, so no
       // wave waits on a longer one
+      // a row group's keys end at its last row's causal limit (prompt rows see fewer)
+      auto group_tokens = [&](int i, int g) {
+        const int rows = nrow[i] * p.G;
+        const int last = std::min(rows, (g + 1) * kAttnRowsPerItem) - 1;
+        return d->ctx_len[i] + last / p.G + 1;
+      };
       auto count_items = [&](int L) {
         int64_t n = 0;
         for (int i = 0; i < p.B; ++i) {
-          const int rows = (d->gamma[i] + 1) * p.G;
-          const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
-          const int64_t pairs = (d->ctx_len[i] + d->gamma[i] + 1 + 31) / 32;
-          n += (int64_t)nrbg * p.nkv * ((pairs + L - 1) / L);
+          const int nrbg = (nrow[i] * p.G + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
+          for (int g = 0; g < nrbg; ++g) {
+            const int64_t pairs = (group_tokens(i, g) + 31) / 32;
+            n += (int64_t)p.nkv * ((pairs + L - 1) / L);
+          }
         }
         return n;
       };
@@ -175,13 +196,13 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
       int L = 2;
       while (L < L_max && count_items(L) > rounds * slots) ++L;
       for (int i = 0; i < p.B; ++i) {
-        const int T = d->ctx_len[i] + d->gamma[i] + 1;
-        const int pairs = (T + 31) / 32;
-        const int n = (pairs + L - 1) / L;
-        const int rows = (d->gamma[i] + 1) * p.G;
+        const int rows = nrow[i] * p.G;
         const int nrbg = (rows + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
         for (int h = 0; h < p.nkv; ++h)
           for (int g = 0; g < nrbg; ++g) {
+            const int T = group_tokens(i, g);
+            const int pairs = (T + 31) / 32;
+            const int n = (pairs + L - 1) / L;
             AttnGroup gr{};
             gr.req = i;
             gr.kvh = h;
@@ -216,19 +237,25 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
   take(p.i_row_pos, p.M);
   take(p.i_items, p.items.size() * 4);
   take(p.i_groups, p.groups.size() * 8);
+  take(p.i_voff, p.B + 1);
+  take(p.i_nrow, p.B);
+  take(p.i_vrow, p.Mv);
   p.host.assign(n, 0);
   for (int i = 0; i <= p.B; ++i) {
     p.host[p.i_off + i] = off[i];
     p.host[p.i_doff + i] = doff[i];
+    p.host[p.i_voff + i] = voff[i];
   }
   for (int i = 0; i < p.B; ++i) {
     p.host[p.i_gamma + i] = d->gamma[i];
     p.host[p.i_ctx + i] = d->ctx_len[i];
     p.host[p.i_req + i] = d->req_id ? (int32_t)d->req_id[i] : i;
-    for (int j = 0; j <= d->gamma[i]; ++j) {
+    p.host[p.i_nrow + i] = nrow[i];
+    for (int j = 0; j < nrow[i]; ++j) {
       p.host[p.i_row_req + off[i] + j] = i;
       p.host[p.i_row_pos + off[i] + j] = d->ctx_len[i] + j;
     }
+    for (int j = 0; j <= d->gamma[i]; ++j) p.host[p.i_vrow + voff[i] + j] = off[i + 1] - (d->gamma[i] + 1) + j;
   }
   if (!p.items.empty()) std::memcpy(&p.host[p.i_items], p.items.data(), p.items.size() * sizeof(AttnItem));
   if (!p.groups.empty()) std::memcpy(&p.host[p.i_groups], p.groups.data(), p.groups.size() * sizeof(AttnGroup));
@@ -238,9 +265,10 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
   carve(p, w, p.w_err, 256);
   carve(p, w, p.w_desc, p.host.size() * sizeof(int32_t));
   const int CH = sampler_chunks(std::max(p.V, 1));
-  carve(p, w, p.w_sm, (size_t)p.M * CH * 4);
-  carve(p, w, p.w_si, (size_t)p.M * CH * 4);
-  carve(p, w, p.w_ss, (size_t)p.M * CH * 8);
+  carve(p, w, p.w_sm, (size_t)p.Mv * CH * 4);
+  carve(p, w, p.w_si, (size_t)p.Mv * CH * 4);
+  carve(p, w, p.w_ss, (size_t)p.Mv * CH * 8);
+  carve(p, w, p.w_vtok, (size_t)(p.prefill ? p.Mv : 0) * 4);
   carve(p, w, p.w_rk, (size_t)p.B * CH * 2 * 4);
   carve(p, w, p.w_ri, (size_t)p.B * CH * 2 * 4);
   carve(p, w, p.w_rR, (size_t)p.B * 4);
@@ -403,6 +431,7 @@ StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_bloc
   sd.req_id = reinterpret_cast<const uint32_t *>(base + p.i_req);
   sd.row_req = base + p.i_row_req;
   sd.row_pos = base + p.i_row_pos;
+  sd.nrow = base + p.i_nrow;
   sd.page_table = d->kv_page_table;
   sd.pt_stride = d->pt_stride;
   sd.n_blocks = n_blocks;
@@ -435,6 +464,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
   const int64_t layer_elems = (int64_t)kv->n_blocks * p.nkv * WISP_PAGE * p.hd;
   const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
   const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
+  const int32_t *vrow = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow;
 
   const double es = p.bf16 ? 2.0 : 4.0;
   auto gemm_bytes = [&](int N, int K) { return es * ((double)N * K + (double)p.M * K) + 4.0 * p.M * N; };
@@ -443,7 +473,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
   double attn_bytes = 0.0, attn_flops = 0.0;
   for (const AttnItem &it : p.items) {
     const int G = p.G;
-    const int rows = (int)p.host[p.i_gamma + it.req] + 1;
+    const int rows = (int)p.host[p.i_nrow + it.req];
     const int rbg = it.kvh_rbg >> 16;
     const int nr = std::min(kAttnRowsPerItem, rows * G - rbg * kAttnRowsPerItem);
     if (rbg == 0) attn_bytes += (double)(it.t1 - it.t0) * kv_tok / p.nkv;
@@ -499,18 +529,23 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
       swiglu<T>(part, sg, af, packed, p.M, p.F, s);
     }
     const int sdn = gemm(af, m->w_down[l], part, p.d, p.F, p.g_down);
-    const T *gain = (l + 1 < m->n_layers) ? (const T *)m->attn_norm[l + 1] : (const T *)m->final_norm;
+    const bool last = l + 1 == m->n_layers;
+    const T *gain = last ? (const T *)m->final_norm : (const T *)m->attn_norm[l + 1];
     {
       ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
-      resid_norm<T>(part, sdn, h, gain, xn, packed, p.M, p.d, m->rms_eps, s);
+      if (last && p.prefill)   // only the verification rows reach the LM head: compact them
+        resid_norm<T>(part, sdn, h, gain, xn, packed, p.M, p.d, m->rms_eps, s, vrow, p.Mv);
+      else
+        resid_norm<T>(part, sdn, h, gain, xn, packed, p.M, p.d, m->rms_eps, s);
     }
   }
   {
-    ProfScope ps(gemm_class(p, p.g_lm), gemm_bytes(p.V, p.d), gemm_flops(p.V, p.d), s);
+    const double lm_bytes = es * ((double)p.V * p.d + (double)p.Mv * p.d) + 4.0 * p.Mv * p.V;
+    ProfScope ps(gemm_class(p, p.g_lm), lm_bytes, 2.0 * p.Mv * p.V * p.d, s);
     if (p.bf16)
-      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.M, p.V, p.d, p.V, p.g_lm, s);
+      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.Mv, p.V, p.d, p.V, p.g_lm, s);
     else
-      gemm_f32((const float *)xn, (const float *)m->lm_head, logits, p.M, p.V, p.d, p.V, s);
+      gemm_f32((const float *)xn, (const float *)m->lm_head, logits, p.Mv, p.V, p.d, p.V, s);
   }
   return hip_check("forward launch");
 }
@@ -585,8 +620,18 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
     st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
   if (st != WISP_OK) return st;
   {
-    ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.M * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
-    sampler(sd, p.B, p.M, p.V, target_logits, tokens, draft_probs, desc->temperature, rng_seed,
+    // the acceptance sees the verification rows only: row offsets over them, and (with
+    // prompt rows present) their tokens gathered into a compact array
+    StepDesc sv = sd;
+    sv.off = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_voff;
+    const int32_t *vtok = tokens;
+    if (p.prefill) {
+      int32_t *g = reinterpret_cast<int32_t *>(ws + p.w_vtok);
+      gather_ints(tokens, reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow, p.Mv, g, s);
+      vtok = g;
+    }
+    ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
+    sampler(sv, p.B, p.Mv, p.V, target_logits, vtok, draft_probs, desc->temperature, rng_seed,
             sampler_scratch(p, ws), accept_len, out_tokens, s);
   }
   return hip_check("sampler launch");

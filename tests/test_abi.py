@@ -49,8 +49,8 @@ def _model(W, **kw):
     return m
 
 
-def _desc(W, ctx, gamma, stride=16, T=1.0):
-    d = W.BatchDesc(ctx, gamma, None, T)
+def _desc(W, ctx, gamma, stride=16, T=1.0, prefill=None):
+    d = W.BatchDesc(ctx, gamma, None, T, prefill_len=prefill)
     d.c.kv_page_table = FAKE
     d.c.pt_stride = stride
     return d
@@ -80,6 +80,23 @@ def test_validation_statuses(W):
     L = W.load_library()
     assert L.wisp_verify(None, None, None, None, None, 0, None, None, None, None, 0, None) == W.WISP_E_INVALID
     assert _verify(W, m, _desc(W, [], [])) == W.WISP_OK          # empty batch: nothing to do
+
+
+def test_prefill_validation_and_sizes(W):
+    """Prompt rows in front of the root: bounds, page capacity over all new rows, and the
+    workspace growing with the forwarded rows while the acceptance sizes stay per draft."""
+    m = _model(W)
+    assert _verify(W, m, _desc(W, [10], [2], prefill=[-1])) == W.WISP_E_INVALID
+    assert "prefill_len" in W.wisp_last_error()
+    assert _verify(W, m, _desc(W, [10], [2], prefill=[32769], stride=4096)) == W.WISP_E_INVALID   # > WISP_PREFILL_MAX
+    # 200 cached + 50 prompt + 2 drafts + root = 253 tokens fit 16 pages; 60 prompt tokens do not
+    assert _verify(W, m, _desc(W, [200], [2], prefill=[60])) == W.WISP_E_CAPACITY
+    base = W.wisp_workspace_size(m, _desc(W, [200], [2]))
+    with_prompt = W.wisp_workspace_size(m, _desc(W, [200], [2], prefill=[50]))
+    assert with_prompt > base > 0
+    assert W.wisp_workspace_size(m, _desc(W, [0], [3], prefill=[0])) == W.wisp_workspace_size(m, _desc(W, [0], [3]))
+    d = _desc(W, [0, 5], [3, 1], prefill=[40, 2])
+    assert d.M == 6 and d.rows == 48
 
 
 def test_workspace_size_and_pack_validation(W):
