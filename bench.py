@@ -35,7 +35,7 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_CLASSES = ((0, "gemm_ring1"), (1, "gemm_ring2"), (2, "gemm_tiled"), (3, "attention"),
                   (4, "attention_combine"), (5, "rows"), (6, "sampler"))
 KERNEL_NAMES = {"gemm_ring1": "gemm_ring_kernel<2, 4, MT/2, 1, 8, 2> (M > 128) / <1, 4, MT, 1, 8, 1>", "gemm_ring2": "gemm_ring_kernel<1, 4, MT, 2, 4, 2>",
-                "gemm_tiled": "gemm_bf16_kernel", "attention": "attn_bf16_kernel",
+                "gemm_tiled": "gemm_f32_kernel", "attention": "attn_bf16_kernel",
                 "attention_combine": "attn_combine_kernel", "rows": "row kernels", "sampler": "sampler kernels"}
 BF16_PEAK_TFLOPS = 2516.6
 FP32_PEAK_TFLOPS = 157.3

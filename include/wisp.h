@@ -213,7 +213,7 @@ wisp_status wisp_check(void *workspace, void *stream);
  */
 #define WISP_PROF_GEMM_RING1 0   /* gemm_ring_kernel, one 32-column fragment per wave (4 or 8 waves) */
 #define WISP_PROF_GEMM_RING2 1   /* gemm_ring_kernel, two 32-column fragments per wave  */
-#define WISP_PROF_GEMM_TILED 2   /* gemm_bf16_kernel (large M) and the fp32 GEMM         */
+#define WISP_PROF_GEMM_TILED 2   /* the fp32 GEMM                                        */
 #define WISP_PROF_ATTN 3         /* attn_bf16_kernel / attn_f32_kernel                   */
 #define WISP_PROF_ATTN_COMBINE 4 /* attn_combine_kernel                                  */
 #define WISP_PROF_ROWS 5         /* embedding, norms, RoPE + KV append, SwiGLU           */

@@ -2,116 +2,18 @@
 //
 // bf16 path: both operands are pre-packed into 32x16 fragments (lane order of gfx950's
 // v_mfma_f32_32x32x16_bf16), so each wave-level load of a fragment is one contiguous
-// 1 KiB read.  A workgroup of four waves stages KS fragments of K per step through
-// double-buffered LDS and accumulates in fp32.  Small-M (the verify step's
-// sum(gamma+1) rows) shapes are HBM-bound on the weight stream; K is split across
-// workgroups when there are too few output tiles to fill the 256 CUs, and the fp32
-// partial sums are added in a fixed order by the consuming epilogue kernel.
+// 1 KiB read.  Every workgroup holds the activations of a block of at most 256 rows
+// (staged through double-buffered LDS) while each wave streams its own weight fragments
+// straight into a register ring, accumulating in fp32.  The verify step's sum(gamma+1)
+// rows make these shapes HBM-bound on the weight stream up to about 315 rows; K is split
+// across workgroups when there are too few output tiles to fill the 256 CUs, and the
+// fp32 partial sums are added in a fixed order by the consuming epilogue kernel.
 #include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
 
 namespace wisp {
-
-template <int WM, int WN, int MT, int NT, int KS>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t *__restrict__ A,
-                                                        const uint16_t *__restrict__ W,
-                                                        float *__restrict__ C, int M, int N, int K,
-                                                        int ldc, int kf_per_split) {
-  constexpr int BMF = WM * MT;        // 32-row fragments of A per tile
-  constexpr int BNF = WN * NT;        // 32-row fragments of W per tile
-  constexpr int A_FR = BMF * KS;
-  constexpr int FR = (BMF + BNF) * KS;
-  constexpr int PER_T = FR * 64 / 256;
-  static_assert((FR * 64) % 256 == 0, "stage must split evenly over 256 threads");
-  __shared__ uint4 lds[2][FR][64];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int KF = K >> 4;
-  const int kf0 = blockIdx.z * kf_per_split;
-  const int kf1 = min(KF, kf0 + kf_per_split);
-  const int nstage = (kf1 - kf0 + KS - 1) / KS;
-  const int rb0 = blockIdx.y * BMF, nb0 = blockIdx.x * BNF;
-  const int MF = (M + 31) >> 5, NF = N >> 5;
-
-  floatx16 acc[MT][NT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < NT; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  uint4 pre[PER_T];
-  auto load_stage = [&](int st) {
-    const int kfs = kf0 + st * KS;
-#pragma unroll
-    for (int t = 0; t < PER_T; ++t) {
-      const int c = tid + 256 * t;
-      const int f = c >> 6, lc = c & 63;
-      if (f < A_FR) {   // compile-time per t: the stage's A pieces come first
-        const int r = rb0 + f / KS, kf = kfs + f % KS;
-        const bool ok = r < MF && kf < kf1;
-        const int rr = ok ? r : 0, kk = ok ? kf : 0;
-        pre[t] = keep_if(ok, ld16(A + (((int64_t)rr * KF + kk) * 64 + lc) * 8));
-      } else {
-        const int g = f - A_FR;   // weights: clamped, unmasked (see gemm_ring_kernel)
-        const int n = min(nb0 + g / KS, NF - 1), kf = min(kfs + g % KS, kf1 - 1);
-        pre[t] = ld16_stream(W + (((int64_t)n * KF + kf) * 64 + lc) * 8);
-      }
-    }
-  };
-  auto store_stage = [&](int buf) {
-#pragma unroll
-    for (int t = 0; t < PER_T; ++t) {
-      const int c = tid + 256 * t;
-      lds[buf][c >> 6][c & 63] = pre[t];
-    }
-  };
-
-  if (nstage > 0) {
-    load_stage(0);
-    store_stage(0);
-  }
-  __syncthreads();
-  for (int st = 0; st < nstage; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nstage) load_stage(st + 1);
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      bf16x8_t a[MT], b[NT];
-#pragma unroll
-      for (int i = 0; i < MT; ++i) a[i] = as_bf16x8(lds[buf][(wm * MT + i) * KS + kk][lane]);
-#pragma unroll
-      for (int j = 0; j < NT; ++j) b[j] = as_bf16x8(lds[buf][A_FR + (wn * NT + j) * KS + kk][lane]);
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (st + 1 < nstage) store_stage(buf ^ 1);
-    __syncthreads();
-  }
-
-  float *Cz = C + (int64_t)blockIdx.z * M * ldc;
-#pragma unroll
-  for (int i = 0; i < MT; ++i) {
-    const int rbase = (rb0 + wm * MT + i) * 32 + 4 * (lane >> 5);
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int col = (nb0 + wn * NT + j) * 32 + (lane & 31);
-      if (col >= N) continue;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = rbase + 8 * (e >> 2) + (e & 3);
-        if (row < M) Cz[(int64_t)row * ldc + col] = acc[i][j][e];
-      }
-    }
-  }
-}
 
 // ---------------------------------------------------------------------------------------
 // Weight-streaming variant for the step's small M: each wave keeps a ring of R weight
@@ -302,52 +204,38 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
   }
 }
 
-static constexpr int kKS = 4;
 static constexpr int kNarrowAD = 1;   // activation prefetch depth of the 32-column ring
 // From this many 32-row fragments on, the 32-column ring runs 8 waves per workgroup (two per
 // SIMD, each on half of the rows), so one wave's products issue while the other waits for
 // memory; below it the extra zero rows and doubled weight requests cost more than that buys
 static constexpr int kPairedWavesMinMT = 5;
-// Up to this many row blocks of <= 256 rows the weight-ring kernels serve any M: each block
-// re-streams the weights, mostly from L2 / MALL while the blocks of a tile run together
-static constexpr int kRingMaxRowBlocks = 8;
 
 // Launch plan.  Weight-ring kernels whose workgroups hold all rows of a row block of at most
 // 256 rows (one block for the verification step's sum(gamma+1) rows at moderate batch
-// sizes, up to kRingMaxRowBlocks blocks beyond); wide outputs use 64-column wave tiles (one
-// A fragment feeds two products), narrow ones 32-column tiles with a deeper ring (8 waves
-// per workgroup from kPairedWavesMinMT row fragments on).  K is split until one workgroup
-// per CU is in flight (one round).  Beyond 2048 rows: the LDS-tiled kernel.
+// sizes; more blocks for larger batches and prompt rows, each re-streaming the weights,
+// mostly from L2 / MALL while the blocks of a tile run together); wide outputs use 64-column
+// wave tiles (one A fragment feeds two products), narrow ones 32-column tiles with a deeper
+// ring (8 waves per workgroup from kPairedWavesMinMT row fragments on).  K is split until
+// one workgroup per CU is in flight (one round).
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
   const int KF = K / 16;
-  int tiles, R;
-  if (mf <= kRingMaxRowBlocks * 8) {
-    // rows in rb blocks of at most 8 fragments, balanced; each block is one grid row of
-    // workgroups that stream the same weights (the grid width is a multiple of 8 for every
-    // projection here, so a tile's row blocks share an XCD and its L2)
-    c.rb = (mf + 7) / 8;
-    int mt = (mf + c.rb - 1) / c.rb;
-    c.kind = N >= 16384 ? 2 : (mt >= kPairedWavesMinMT ? 3 : 1);
-    if (c.kind == 3 && c.rb > 1) mt += mt & 1;   // paired halves: a block is 2 * ceil(mt / 2) fragments
-    c.mt = mt;
-    c.bm = 32 * mt;
-    c.bn = c.kind == 2 ? 256 : 128;
-    R = c.kind == 2 ? 4 : 8;
-    tiles = ((N + c.bn - 1) / c.bn) * c.rb;
-  } else {
-    c.kind = 0;
-    c.mt = 0;
-    c.rb = (M + 255) / 256;
-    c.bm = 256;
-    c.bn = 128;
-    R = kKS;
-    tiles = ((N + c.bn - 1) / c.bn) * c.rb;
-  }
+  // rows in rb blocks of at most 8 fragments, balanced; each block is one grid row of
+  // workgroups that stream the same weights (the grid width is a multiple of 8 for every
+  // projection here, so a tile's row blocks share an XCD and its L2)
+  c.rb = (mf + 7) / 8;
+  int mt = (mf + c.rb - 1) / c.rb;
+  c.kind = N >= 16384 ? 2 : (mt >= kPairedWavesMinMT ? 3 : 1);
+  if (c.kind == 3 && c.rb > 1) mt += mt & 1;   // paired halves: a block is 2 * ceil(mt / 2) fragments
+  c.mt = mt;
+  c.bm = 32 * mt;
+  c.bn = c.kind == 2 ? 256 : 128;
+  const int R = c.kind == 2 ? 4 : 8;
+  const int tiles = ((N + c.bn - 1) / c.bn) * c.rb;
   // workgroups resident at once: the ring kernels hold one workgroup per CU (LDS and
   // registers), so more than one round of 256 would leave a partial second round
-  const int max_wg = c.kind == 0 ? 384 : 256;
+  const int max_wg = 256;
   int splits = 1;
   while (splits < 16 && tiles * splits * 2 <= max_wg && KF / (splits * 2) >= 4 * R) splits *= 2;
   int kps = (KF + splits - 1) / splits;
@@ -386,11 +274,6 @@ static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W,
 
 void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
                const GemmCfg &cfg, hipStream_t s) {
-  if (cfg.kind == 0) {
-    dim3 grid((N + cfg.bn - 1) / cfg.bn, (M + cfg.bm - 1) / cfg.bm, cfg.splits);
-    launch(gemm_bf16_kernel<2, 2, 4, 2, kKS>, grid, 256, 0, s, A, W, C, M, N, K, ldc, cfg.kf_per_split);
-    return;
-  }
   dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, cfg.rb, 1);
   if (cfg.kind == 1)
     launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);

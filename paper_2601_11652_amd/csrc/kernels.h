@@ -24,10 +24,10 @@ inline void launch(void (*kernel)(Formals...), dim3 grid, dim3 block, uint32_t s
 
 // ----- GEMMs: C[z][M][ldc] (fp32) = A[M][K] . W[N][K]^T over the z-th K range ----------
 struct GemmCfg {
-  int kind;         // 0: LDS-tiled (any M), 1: weight ring NT=1 R=8, 2: weight ring NT=2 R=4,
+  int kind;         // 1: weight ring NT=1 R=8, 2: weight ring NT=2 R=4,
                     // 3: weight ring NT=1 R=8 with 8 waves (two per SIMD on half the rows each)
-  int mt;           // ring kinds: 32-row fragments of A held by every workgroup
-  int rb;           // row blocks (grid rows); ring kinds: rb * mt fragments cover ceil(M/32)
+  int mt;           // 32-row fragments of A held by every workgroup
+  int rb;           // row blocks (grid rows): rb * mt fragments cover ceil(M/32)
   int bm, bn;       // tile rows / cols
   int splits;       // K splits (partial sums in fp32, summed in fixed order later)
   int kf_per_split; // 16-wide K fragments per split

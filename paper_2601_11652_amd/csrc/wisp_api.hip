@@ -440,7 +440,7 @@ StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_bloc
 }
 
 int gemm_class(const Plan &p, const GemmCfg &c) {
-  if (!p.bf16 || c.kind == 0) return WISP_PROF_GEMM_TILED;
+  if (!p.bf16) return WISP_PROF_GEMM_TILED;
   return c.kind == 2 ? WISP_PROF_GEMM_RING2 : WISP_PROF_GEMM_RING1;
 }
 

@@ -28,10 +28,15 @@ import numpy as np
 FEATURES = ("N_linear", "N_interactions", "N_cached")
 
 
-def step_features(ctx_len, gamma) -> np.ndarray:
-    """[N_linear, N_interactions, N_cached] of one verification batch (Sec. 4.4)."""
+def step_features(ctx_len, gamma, prefill_len=None) -> np.ndarray:
+    """[N_linear, N_interactions, N_cached] of one verification batch (Sec. 4.4): request i
+    brings L_new = prefill_len + gamma + 1 new tokens (its uncached prompt, root and drafts)
+    on top of L_cached = ctx_len cached ones; N_linear = sum L_new, N_interactions =
+    sum (L_cached + L_new) * L_new, N_cached = sum L_cached."""
     ctx = np.asarray(ctx_len, dtype=np.float64)
     new = np.asarray(gamma, dtype=np.float64) + 1.0
+    if prefill_len is not None:
+        new = new + np.asarray(prefill_len, dtype=np.float64)
     return np.array([new.sum(), ((ctx + new) * new).sum(), ctx.sum()])
 
 

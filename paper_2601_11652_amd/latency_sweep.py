@@ -1,25 +1,27 @@
 """Profiling sweep that fits the verification-time estimator on this GPU (Sec. 4.4, App. C).
 
 The paper fits T_hat = a * N_linear + b_compute * N_interactions + b_read * N_cached + c
-to measured verification latencies over five categories of batches (App. C): a
-compute-bound group (large batches of short requests), a memory-bound grid, two groups of
-random draws, and mixed long/short batches.  Here the five categories are rebuilt for
-drafts of at most 16 tokens:
+to measured verification latencies.  The configurations follow App. C's design, with
+request i's L_new new tokens realised as prefill_len uncached prompt tokens, the root and
+gamma = min(L_new - 1, 5) drafts (a first-time verification when nothing is cached):
 
-  1. compute-bound: B in {64, 128, 256}, ctx in {64, 256}, gamma in {4, 8, 16};
-  2. memory-bound grid: gamma + 1 in {1, 2, 5, 9, 17} x ctx in {512, 2048, 8192, 32768}
-     x B in {1, 4, 32};
-  3. random homogeneous: B ~ U{1..64}, one ctx ~ logU[128, 16384] and one gamma ~
-     U{0..16} per batch;
-  4. random heterogeneous: per-request ctx ~ logU[128, 16384], gamma ~ U{0..16};
-  5. mixed: half the requests long (ctx ~ U[16384, 32768]), half short (ctx ~
-     U[128, 512]), gamma ~ U{1..8}.
+Training set (123):
+  1. 25 compute-bound deterministic: L_cached = 0 and 1200 .. 2000 new tokens in total,
+     as one request, 2, 3 or 4 equal requests, or 3 unequal ones (50 / 30 / 20 %);
+  2. 48 memory-bound deterministic: L_new in {1, 5, 10, 20, 50, 100} x L_total in
+     {500, 1000, 1500, 2000} x B in {1, 4}, L_cached = L_total - L_new;
+  3. 15 compute-bound random: 1 .. 4 requests, L_new >= 1200 in total, small caches;
+  4. 15 memory-bound random: 1 .. 8 requests, L_new 1 .. 20, L_total 1000 .. 4000;
+  5. 20 mixed: 1 .. 2 uncached requests (L_new 200 .. 1000) batched with 2 .. 8 cached
+     follow-ups (L_new 2 .. 9, L_cached 500 .. 4000).
+Test set (50, never seen by the fit): 10 / 15 / 25 draws of categories 3 / 4 / 5 from a
+different seed.
 
 Each configuration is timed as App. C does: 10 warm-up steps, then 3 timed steps (HIP
 events on the calling stream); the coefficient of variation of the 3 is recorded.  Inputs
-are synthetic (the KV content and the drafts do not change the step's work).  The split
-into 123 training and 50 test configurations is seeded and disjoint; the fit follows the
-App. C protocol (OLS, 1000-sample bootstrap 95% intervals, 5-fold cross-validation).
+are synthetic (the KV content and the tokens do not change the step's work).  The fit
+follows the App. C protocol (OLS, 1000-sample bootstrap 95% intervals, 5-fold
+cross-validation).
 
 Run on a GPU:  python -m paper_2601_11652_amd.latency_sweep --out profiles/latency_model_8b.json
 """
@@ -30,68 +32,90 @@ import json
 import os
 import sys
 import time
-from dataclasses import dataclass, asdict
+from dataclasses import dataclass
 
 import numpy as np
 
 from .latency_model import fit_report, step_features
 
 PAGE = 16
+DRAFTS = 5
 
 
 @dataclass
 class SweepConfig:
     cid: int
     category: int
-    ctx_len: list
-    gamma: list
+    split: str          # "train" or "test"
+    ctx_len: list       # L_cached per request
+    l_new: list         # L_new per request (prompt + root + drafts)
 
     @property
     def B(self) -> int:
-        return len(self.gamma)
+        return len(self.l_new)
+
+    @property
+    def gamma(self) -> list:
+        return [min(n - 1, DRAFTS) for n in self.l_new]
+
+    @property
+    def prefill_len(self) -> list:
+        return [n - 1 - g for n, g in zip(self.l_new, self.gamma)]
 
 
-def sweep_configs(seed: int = 20260111) -> list:
-    """The ~173 configurations of the five categories, deterministic in `seed`."""
-    rng = np.random.default_rng(seed)
+def _random_configs(rng, cat: int):
+    if cat == 3:
+        B = int(rng.integers(1, 5))
+        total = int(rng.integers(1200, 2401))
+        w = rng.dirichlet(np.ones(B))
+        new = np.maximum(1, np.round(w * total)).astype(int)
+        return rng.integers(0, 201, size=B), new
+    if cat == 4:
+        B = int(rng.integers(1, 9))
+        new = rng.integers(1, 21, size=B)
+        tot = rng.integers(1000, 4001, size=B)
+        return tot - new, new
+    n_cold = int(rng.integers(1, 3))
+    n_warm = int(rng.integers(2, 9))
+    ctx = np.concatenate([np.zeros(n_cold, int), rng.integers(500, 4001, size=n_warm)])
+    new = np.concatenate([rng.integers(200, 1001, size=n_cold), rng.integers(2, 10, size=n_warm)])
+    perm = rng.permutation(n_cold + n_warm)
+    return ctx[perm], new[perm]
+
+
+def sweep_configs(seed: int = 20260111, test_seed: int = 7) -> list:
+    """The 173 configurations (123 training, 50 test), deterministic in the seeds."""
     out = []
 
-    def add(cat, ctx, gam):
-        out.append(SweepConfig(len(out), cat, [int(c) for c in ctx], [int(g) for g in gam]))
+    def add(cat, split, ctx, new):
+        out.append(SweepConfig(len(out), cat, split, [int(c) for c in ctx], [int(n) for n in new]))
 
-    for B in (64, 128, 256):                                   # 1: compute-bound
-        for ctx in (64, 256):
-            for g in (4, 8, 16):
-                add(1, [ctx] * B, [g] * B)
-    for new in (1, 2, 5, 9, 17):                               # 2: memory-bound grid
-        for ctx in (512, 2048, 8192, 32768):
-            for B in (1, 4, 32):
-                add(2, [ctx] * B, [new - 1] * B)
-    for _ in range(35):                                        # 3: random homogeneous
-        B = int(rng.integers(1, 65))
-        ctx = int(np.exp(rng.uniform(np.log(128), np.log(16384))))
-        add(3, [ctx] * B, [int(rng.integers(0, 17))] * B)
-    for _ in range(35):                                        # 4: random heterogeneous
-        B = int(rng.integers(1, 65))
-        ctx = np.exp(rng.uniform(np.log(128), np.log(16384), size=B)).astype(int)
-        add(4, ctx, rng.integers(0, 17, size=B))
-    for _ in range(25):                                        # 5: mixed long / short
-        B = int(rng.integers(2, 33))
-        n_long = B // 2
-        ctx = np.concatenate([rng.integers(16384, 32769, size=n_long), rng.integers(128, 513, size=B - n_long)])
-        add(5, rng.permutation(ctx), rng.integers(1, 9, size=B))
+    for total in (1200, 1400, 1600, 1800, 2000):                       # 1: compute-bound
+        for parts in ([1.0], [0.5, 0.5], [1 / 3] * 3, [0.25] * 4, [0.5, 0.3, 0.2]):
+            new = [int(total * f) for f in parts]
+            new[-1] += total - sum(new)
+            add(1, "train", [0] * len(new), new)
+    for l_new in (1, 5, 10, 20, 50, 100):                              # 2: memory-bound grid
+        for l_tot in (500, 1000, 1500, 2000):
+            for B in (1, 4):
+                add(2, "train", [l_tot - l_new] * B, [l_new] * B)
+    rng = np.random.default_rng(seed)
+    for cat, n in ((3, 15), (4, 15), (5, 20)):
+        for _ in range(n):
+            add(cat, "train", *_random_configs(rng, cat))
+    rng = np.random.default_rng(test_seed)
+    for cat, n in ((3, 10), (4, 15), (5, 25)):
+        for _ in range(n):
+            add(cat, "test", *_random_configs(rng, cat))
     return out
 
 
-def train_test_split(configs, n_test: int = 50, seed: int = 7):
-    """Seeded, disjoint split of configuration ids."""
-    idx = np.random.default_rng(seed).permutation(len(configs))
-    test = set(int(i) for i in idx[:n_test])
-    return [c for c in configs if c.cid not in test], [c for c in configs if c.cid in test]
+def train_test_split(configs):
+    return [c for c in configs if c.split == "train"], [c for c in configs if c.split == "test"]
 
 
 def features(configs) -> np.ndarray:
-    return np.stack([step_features(c.ctx_len, c.gamma) for c in configs])
+    return np.stack([step_features(c.ctx_len, c.gamma, c.prefill_len) for c in configs])
 
 
 def measure(configs, shape, seed: int = 1, warmup: int = 10, runs: int = 3, log=print):
@@ -103,7 +127,7 @@ def measure(configs, shape, seed: int = 1, warmup: int = 10, runs: int = 3, log=
 
     torch.cuda.set_device(0)
     gm = GpuModel(shape, lambda l: wi.layer_weights(shape, l, seed, "cuda"), wi.global_weights(shape, seed, "cuda"))
-    pages = max(sum((c + g + 1 + PAGE - 1) // PAGE for c, g in zip(cf.ctx_len, cf.gamma)) for cf in configs)
+    pages = max(sum((c + n + PAGE - 1) // PAGE for c, n in zip(cf.ctx_len, cf.l_new)) for cf in configs)
     dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
     kv = KVPool.zeros(shape.n_layers, pages, shape.n_kv_heads, shape.head_dim, dt)
     log(f"KV pool of {pages} pages ({2 * kv.k.numel() * kv.k.element_size() / 2**30:.1f} GiB)")
@@ -115,18 +139,18 @@ def measure(configs, shape, seed: int = 1, warmup: int = 10, runs: int = 3, log=
     for cf in configs:
         ctx = np.asarray(cf.ctx_len, np.int32)
         gam = np.asarray(cf.gamma, np.int32)
-        need = (ctx + gam + 1 + PAGE - 1) // PAGE
+        pre = np.asarray(cf.prefill_len, np.int32)
+        need = (ctx + np.asarray(cf.l_new) + PAGE - 1) // PAGE
         pt = torch.full((cf.B, int(need.max())), -1, dtype=torch.int32)
         o = 0
         for i in range(cf.B):
             pt[i, :need[i]] = perm[o:o + need[i]]
             o += int(need[i])
         pt = pt.cuda()
-        M = int((gam + 1).sum())
-        S = int(gam.sum())
-        tokens = torch.randint(0, shape.vocab, (M,), dtype=torch.int32, device="cuda", generator=gen)
+        desc = BatchDesc(ctx, gam, pt, 1.0, np.arange(cf.B, dtype=np.uint32), prefill_len=pre)
+        M, S = desc.M, desc.S
+        tokens = torch.randint(0, shape.vocab, (desc.rows,), dtype=torch.int32, device="cuda", generator=gen)
         q = torch.softmax(torch.randn(max(S, 1), shape.vocab, device="cuda", generator=gen), dim=-1)
-        desc = BatchDesc(ctx, gam, pt, 1.0, np.arange(cf.B, dtype=np.uint32))
         ws = workspace(wisp_workspace_size(gm.c, desc))
         acc = torch.empty(cf.B, dtype=torch.int32, device="cuda")
         out = torch.empty(M, dtype=torch.int32, device="cuda")
@@ -142,20 +166,20 @@ def measure(configs, shape, seed: int = 1, warmup: int = 10, runs: int = 3, log=
             e1.synchronize()
             ts.append(e0.elapsed_time(e1))
         ts = np.asarray(ts)
-        f = step_features(ctx, gam)
-        rows.append({"cid": cf.cid, "category": cf.category, "B": cf.B, "M": M,
+        f = step_features(ctx, gam, pre)
+        rows.append({"cid": cf.cid, "category": cf.category, "split": cf.split, "B": cf.B, "rows": desc.rows,
                      "N_linear": float(f[0]), "N_interactions": float(f[1]), "N_cached": float(f[2]),
                      "ms_mean": float(ts.mean()), "ms_cv": float(ts.std() / ts.mean())})
-        log(f"config {cf.cid:3d} (cat {cf.category}, B {cf.B:3d}, M {M:4d}, cached {int(f[2]):8d}): "
-            f"{ts.mean():8.3f} ms  cv {100 * ts.std() / ts.mean():4.1f} %")
+        log(f"config {cf.cid:3d} ({cf.split}, cat {cf.category}, B {cf.B:2d}, new {int(f[0]):5d}, cached "
+            f"{int(f[2]):6d}): {ts.mean():8.3f} ms  cv {100 * ts.std() / ts.mean():4.1f} %")
         del ws, logits, q
     return rows
 
 
-def fit(rows, configs, n_test: int = 50, seed: int = 7) -> dict:
+def fit(rows, configs) -> dict:
     """App. C fit on the measured rows (seconds, like the paper's coefficients)."""
     by_id = {r["cid"]: r for r in rows}
-    train, test = train_test_split(configs, n_test, seed)
+    train, test = train_test_split(configs)
 
     def xy(cs):
         X = np.array([[by_id[c.cid]["N_linear"], by_id[c.cid]["N_interactions"], by_id[c.cid]["N_cached"]] for c in cs])
@@ -183,7 +207,7 @@ def main(argv=None):
         configs = configs[:args.limit]
     t0 = time.time()
     rows = measure(configs, shape, log=lambda m: print(m, flush=True))
-    rep = fit(rows, configs, n_test=min(50, len(configs) // 3))
+    rep = fit(rows, configs)
     rec = {"model": shape.name, "protocol": "10 warm-up + 3 timed steps per configuration (App. C)",
            "fit": rep, "rows": rows, "seconds": time.time() - t0}
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)

@@ -8,7 +8,7 @@
 * a batch of plain-decode requests only (no draft rows; the draft distributions may be
   NULL);
 * more than 256 rows (24 requests x 17 rows = 408), which the weight-ring GEMMs serve in
-  two row blocks, and more than 2048 rows (124 x 17 = 2108), which takes the LDS-tiled GEMM;
+  two row blocks, and 2108 rows (124 x 17) in nine;
 * 129-256 rows, where the 32-column weight-ring GEMM runs 8 waves on two row halves: an
   odd number of 32-row fragments (150 rows: one half carries a zero fragment) and an even
   one (192 rows);
@@ -130,7 +130,7 @@ def test_more_than_256_rows_in_row_blocks():
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs, 6e-2)
 
 
-def test_more_than_2048_rows_takes_the_tiled_gemm():
+def test_2108_rows_in_nine_row_blocks():
     B = 124
     ctx = [int(c) for c in np.random.default_rng(6).integers(0, 40, size=B)]
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs, 6e-2)

@@ -62,23 +62,39 @@ def test_fit_report_protocol():
 
 
 def test_sweep_configurations():
-    """The profiling sweep: 173 configurations in the five categories, deterministic,
-    gamma <= 16, and a disjoint 123 / 50 train / test split."""
+    """The profiling sweep follows App. C: 123 training configurations in five categories
+    (25 compute-bound with nothing cached and 1200 .. 2000 new tokens, the 48-point
+    memory-bound grid, 15 + 15 random ones of each regime, 20 mixed cached / uncached) and
+    50 unseen test configurations; deterministic; L_new realised as prompt + root + drafts
+    with at most 5 drafts."""
     from paper_2601_11652_amd import latency_sweep as ls
     a = ls.sweep_configs()
     b = ls.sweep_configs()
     assert len(a) == 173
-    assert [(c.ctx_len, c.gamma) for c in a] == [(c.ctx_len, c.gamma) for c in b]
-    counts = {k: sum(c.category == k for c in a) for k in range(1, 6)}
-    assert counts == {1: 18, 2: 60, 3: 35, 4: 35, 5: 25}
-    for c in a:
-        assert len(c.ctx_len) == len(c.gamma) >= 1
-        assert max(c.gamma) <= 16 and min(c.gamma) >= 0 and min(c.ctx_len) >= 1
+    assert [(c.ctx_len, c.l_new) for c in a] == [(c.ctx_len, c.l_new) for c in b]
     tr, te = ls.train_test_split(a)
     assert len(tr) == 123 and len(te) == 50
-    assert not {c.cid for c in tr} & {c.cid for c in te}
+    counts = {k: sum(c.category == k for c in tr) for k in range(1, 6)}
+    assert counts == {1: 25, 2: 48, 3: 15, 4: 15, 5: 20}
+    assert {k: sum(c.category == k for c in te) for k in range(1, 6)} == {1: 0, 2: 0, 3: 10, 4: 15, 5: 25}
+    for c in a:
+        assert len(c.ctx_len) == len(c.l_new) >= 1 and min(c.l_new) >= 1 and min(c.ctx_len) >= 0
+        assert all(0 <= g <= 5 and p >= 0 and p + g + 1 == n for g, p, n in zip(c.gamma, c.prefill_len, c.l_new))
+    for c in tr:
+        if c.category == 1:
+            assert sum(c.ctx_len) == 0 and 1200 <= sum(c.l_new) <= 2000
+        if c.category == 2:
+            assert len(set(c.l_new)) == 1 and c.l_new[0] in (1, 5, 10, 20, 50, 100)
+            assert c.ctx_len[0] + c.l_new[0] in (500, 1000, 1500, 2000) and c.B in (1, 4)
+        if c.category == 5:
+            assert min(c.ctx_len) == 0 and max(c.ctx_len) >= 500
     X = ls.features(a)
     assert X.shape == (173, 3) and np.all(np.isfinite(X))
-    # N_interactions >= N_linear (every new row sees at least itself), N_cached = sum ctx
+    # N_interactions >= N_linear (every new token sees at least itself); N_cached = sum ctx;
+    # N_linear = sum L_new
     assert np.all(X[:, 1] >= X[:, 0])
     assert np.allclose(X[:, 2], [sum(c.ctx_len) for c in a])
+    assert np.allclose(X[:, 0], [sum(c.l_new) for c in a])
+    # a cold start's interactions are quadratic in its new tokens
+    cold = ls.step_features([0], [5], [94])
+    assert cold[0] == 100 and cold[1] == 100 * 100 and cold[2] == 0
