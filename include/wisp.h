@@ -202,9 +202,10 @@ wisp_status wisp_check(void *workspace, void *stream);
 
 /*
  * Opt-in timing of wisp_verify's kernels by kernel (instrumentation for benchmarks; off by
- * default, process-wide, not thread-safe).  While enabled, each launch of a class is
- * bracketed by HIP events on the caller's stream, and the class accumulates the measured
- * milliseconds, the launch count and the algorithmic bytes / flops of its launches:
+ * default, process-wide, not thread-safe).  While enabled, each launch of a class gets a
+ * pair of HIP events on the caller's stream that the runtime stamps with the dispatch's own
+ * begin and end, and the class accumulates the measured milliseconds, the launch count and
+ * the algorithmic bytes / flops of its launches:
  *   GEMM classes: 2-byte (bf16) or 4-byte weights N*K + activations M*K + fp32 result M*N;
  *   ATTN: K and V bytes of every token each kv head reads (ctx_len + gamma + 1 per request);
  *   SAMPLER: two passes over the fp32 logits plus one row per request;
@@ -222,6 +223,53 @@ wisp_status wisp_check(void *workspace, void *stream);
 wisp_status wisp_profile_enable(int on);
 wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops);
 wisp_status wisp_profile_reset(void);
+
+/*
+ * Verification batch scheduling (Sec. 4.3, Alg. 1), host code.
+ *
+ * Batch-time estimator of Sec. 4.4 (seconds):
+ *   T(B) = a * N_linear + b_compute * N_interactions + b_read * N_cached + c,
+ *   N_linear = sum L_new, N_interactions = sum (L_cached + L_new) * L_new,
+ *   N_cached = sum L_cached over the requests of B.
+ * A pending request carries its deadline d_i = a_i + tau_c(i) (Sec. 4.3, with the
+ * server budget tau of the class), its expected verified tokens g_i = alpha_i * N_d,i
+ * (the verified-token estimate of Sec. 3), its memory footprint m_i and its L_cached,
+ * L_new.  Its verification cost is v_i = T({i}), its utility U_i = g_i / v_i and its
+ * latest start time LST_i = d_i - v_i - guard (Sec. 4.3).
+ *
+ * wisp_schedule picks the batch dispatched at time t_now from the n pending requests:
+ *   WISP_SCHED_SLO  Alg. 1: requests with t_now >= LST_i ("critical") in increasing d_i,
+ *                   then the others in decreasing U_i (ties: lower index first), each
+ *                   admitted while the batch stays feasible (sum m <= mem_budget and
+ *                   t_now + T(batch) <= min d over the batch); the first infeasible
+ *                   admission ends the batch, and a critical one also skips the others.
+ *                   If no request can be admitted, the first critical request (or, with
+ *                   none, the highest-utility one) is dispatched alone when it fits in
+ *                   memory: a request past saving is still verified, by itself.
+ *   WISP_SCHED_FCFS requests in increasing arrival time (ties: lower index first) while
+ *                   sum m <= mem_budget (the scheduler disabled: no deadline test).
+ * batch receives the chosen request indices in admission order (capacity n), batch_len
+ * their count (0 when nothing fits).  Errors: WISP_E_INVALID for NULL pointers, n < 0, an
+ * unknown policy or a request with l_new < 1 or ctx_len < 0.
+ */
+typedef struct {
+  double a, b_compute, b_read, c;
+} wisp_latency_model;
+
+typedef struct {
+  double arrival;   /* a_i, seconds                                                           */
+  double deadline;  /* d_i, seconds (same clock)                                              */
+  double g_hat;     /* expected verified tokens                                               */
+  double m_hat;     /* memory footprint, in the unit of mem_budget                            */
+  int32_t ctx_len;  /* L_cached                                                               */
+  int32_t l_new;    /* L_new (prompt rows + root + drafts)                                    */
+} wisp_sched_request;
+
+#define WISP_SCHED_SLO 0
+#define WISP_SCHED_FCFS 1
+wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *requests, int32_t n, double t_now,
+                          double mem_budget, double guard, const wisp_latency_model *model,
+                          int32_t *batch, int32_t *batch_len);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char *wisp_last_error(void);

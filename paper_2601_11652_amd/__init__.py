@@ -7,7 +7,7 @@ the library has not been built -- there is no fallback implementation.
 
 Entry points keep the C names: wisp_verify, wisp_accept, wisp_attention,
 wisp_pack_linear, wisp_workspace_size, wisp_accept_workspace_size, wisp_uniform,
-wisp_check, wisp_last_error.  ``GpuModel`` and ``make_desc`` assemble the C structs.
+wisp_check, wisp_last_error, wisp_schedule.  ``GpuModel`` and ``BatchDesc`` assemble the C structs.
 """
 from __future__ import annotations
 
@@ -35,7 +35,7 @@ TAG_RACE = 2
 
 EXPORTS = ("wisp_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
            "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
-           "wisp_profile_read", "wisp_profile_reset", "wisp_last_error")
+           "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule")
 
 
 class WispError(RuntimeError):
@@ -66,6 +66,18 @@ class wisp_batch_desc(C.Structure):
                 ("req_id", C.POINTER(C.c_uint32)), ("kv_page_table", _VP), ("pt_stride", C.c_int32),
                 ("temperature", C.c_float), ("prefill_len", C.POINTER(C.c_int32))]
 
+
+class wisp_latency_model(C.Structure):
+    _fields_ = [("a", C.c_double), ("b_compute", C.c_double), ("b_read", C.c_double), ("c", C.c_double)]
+
+
+class wisp_sched_request(C.Structure):
+    _fields_ = [("arrival", C.c_double), ("deadline", C.c_double), ("g_hat", C.c_double),
+                ("m_hat", C.c_double), ("ctx_len", C.c_int32), ("l_new", C.c_int32)]
+
+
+WISP_SCHED_SLO = 0
+WISP_SCHED_FCFS = 1
 
 _lib = None
 
@@ -102,8 +114,12 @@ def _load():
     L.wisp_profile_reset.argtypes = []
     L.wisp_last_error.argtypes = []
     L.wisp_last_error.restype = C.c_char_p
+    L.wisp_schedule.argtypes = [C.c_int32, C.POINTER(wisp_sched_request), C.c_int32, C.c_double, C.c_double,
+                                C.c_double, C.POINTER(wisp_latency_model), C.POINTER(C.c_int32),
+                                C.POINTER(C.c_int32)]
     for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
-                 "wisp_check", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset"):
+                 "wisp_check", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
+                 "wisp_schedule"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -307,6 +323,21 @@ def wisp_attention(model: wisp_model, kv: KVPool, desc: BatchDesc, q, out, works
 
 def wisp_uniform(rng_seed: int, req_id: int, tag: int, row: int, n: int, out, stream=None):
     _ok(lib.wisp_uniform(rng_seed & ((1 << 64) - 1), req_id, tag, row, n, _ptr(out), _stream(stream)))
+
+
+def wisp_schedule(policy: int, requests, t_now: float, mem_budget: float, guard: float, model) -> list:
+    """Batch for the dispatch epoch t_now (Sec. 4.3, Alg. 1; host code).  requests: sequence of
+    objects with arrival, deadline, g_hat, m_hat, ctx_len, l_new; model: (a, b_compute,
+    b_read, c) in seconds.  Returns the admitted request indices in admission order."""
+    n = len(requests)
+    arr = (wisp_sched_request * max(n, 1))()
+    for i, r in enumerate(requests):
+        arr[i] = wisp_sched_request(r.arrival, r.deadline, r.g_hat, r.m_hat, r.ctx_len, r.l_new)
+    out = (C.c_int32 * max(n, 1))()
+    k = C.c_int32(0)
+    m = wisp_latency_model(*[float(x) for x in model])
+    _ok(lib.wisp_schedule(policy, arr, n, t_now, mem_budget, guard, C.byref(m), out, C.byref(k)))
+    return list(out[:k.value])
 
 
 def wisp_check(workspace, stream=None):

@@ -552,6 +552,11 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
 
 }  // namespace
 
+namespace wisp {
+// lets the host-only sources (the scheduler) report through wisp_last_error
+wisp_status report_error(wisp_status st, const char *msg) { return fail(st, "%s", msg); }
+}  // namespace wisp
+
 // ------------------------------------------------------------------------------------------
 // exported entry points
 // ------------------------------------------------------------------------------------------
