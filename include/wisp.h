@@ -243,9 +243,12 @@ wisp_status wisp_profile_reset(void);
  *                   admitted while the batch stays feasible (sum m <= mem_budget and
  *                   t_now + T(batch) <= min d over the batch); the first infeasible
  *                   admission ends the batch, and a critical one also skips the others.
- *                   If no request can be admitted, the first critical request (or, with
- *                   none, the highest-utility one) is dispatched alone when it fits in
- *                   memory: a request past saving is still verified, by itself.
+ *                   A request with t_now + v_i > d_i has lost its deadline already: it
+ *                   keeps its place in deadline order and counts against memory, but its
+ *                   d_i is left out of the min (as printed, it would end every batch
+ *                   before any admission and the queue would stall).  A request whose
+ *                   m_i alone exceeds mem_budget is never admitted: the caller turns it
+ *                   away.
  *   WISP_SCHED_FCFS requests in increasing arrival time (ties: lower index first) while
  *                   sum m <= mem_budget (the scheduler disabled: no deadline test).
  * batch receives the chosen request indices in admission order (capacity n), batch_len

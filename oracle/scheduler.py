@@ -8,8 +8,14 @@ batch-time estimator of Sec. 4.4, and the first failed check ends the batch (a f
 critical admission also skips the utility fill).  Readings where the paper is silent:
   * the verification cost v_i of a request is the estimator's time for the request alone;
   * ties keep the lower request index first (both orderings are stable);
-  * when no request can be admitted, the first critical request (else the top-utility one)
-    is dispatched alone if it fits in memory, so a request past saving is still verified;
+  * a request that misses its deadline even when verified alone (t + v_i > d_i) has lost
+    its SLO already, and no batch can satisfy the deadline constraint for it: its deadline
+    is left out of the batch's tightest deadline.  It keeps its place in the critical
+    queue (its deadline is among the earliest) and is still checked against memory.  As
+    printed, such a request would end every batch before anything is admitted, and the
+    queue would never move again;
+  * a request whose memory alone exceeds the budget is never admitted (the caller has to
+    turn it away);
   * FCFS (the scheduler disabled) takes requests in arrival order while memory fits.
 Only tests and the benchmarks' baselines may import this module.
 """
@@ -53,13 +59,18 @@ def schedule_slo(reqs, t_now: float, mem_budget: float, guard: float, model) -> 
     critical.sort(key=lambda i: reqs[i].deadline)          # EDF (stable)
     others.sort(key=lambda i: -utility[i])                  # by decreasing utility (stable)
 
+    expired = [t_now + v[i] > reqs[i].deadline for i in range(n)]
+
     batch: list = []
     mem = 0.0
 
     def feasible_add(i) -> bool:
-        members = [reqs[j] for j in batch] + [reqs[i]]
-        d_min = min(r.deadline for r in members)
-        return mem + reqs[i].m_hat <= mem_budget and t_now + batch_time(model, members) <= d_min
+        members = batch + [i]
+        fits = mem + reqs[i].m_hat <= mem_budget
+        live = [reqs[j].deadline for j in members if not expired[j]]
+        if not live:
+            return fits
+        return fits and t_now + batch_time(model, [reqs[j] for j in members]) <= min(live)
 
     stop = False
     for i in critical:
@@ -76,10 +87,6 @@ def schedule_slo(reqs, t_now: float, mem_budget: float, guard: float, model) -> 
                 batch.append(i)
             else:
                 break
-    if not batch:
-        head = critical[0] if critical else others[0]
-        if reqs[head].m_hat <= mem_budget:
-            batch.append(head)
     return batch
 
 

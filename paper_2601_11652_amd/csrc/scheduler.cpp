@@ -39,22 +39,30 @@ struct Batch {
   const wisp_sched_request *q;
   const wisp_latency_model &m;
   double t_now, budget;
+  const std::vector<char> &expired;   // t_now + v_i > d_i: the deadline is lost already
   Features f;
   double mem = 0.0, dmin = 0.0;
+  bool live = false;                    // some member's deadline can still be met
   std::vector<int32_t> members;
 
-  // FeasibleAdd of Alg. 1: memory and the tightest deadline with i included
+  // FeasibleAdd of Alg. 1: memory, and the tightest deadline among members whose deadline
+  // is not lost already, with i included
   bool feasible_with(int32_t i) const {
+    if (!(mem + q[i].m_hat <= budget)) return false;
+    const bool live2 = live || !expired[i];
+    if (!live2) return true;
+    const double d2 = expired[i] ? dmin : (live ? std::min(dmin, q[i].deadline) : q[i].deadline);
     Features g = f;
     g.add(q[i]);
-    const double mem2 = mem + q[i].m_hat;
-    const double d2 = members.empty() ? q[i].deadline : std::min(dmin, q[i].deadline);
-    return mem2 <= budget && t_now + batch_time(m, g) <= d2;
+    return t_now + batch_time(m, g) <= d2;
   }
   void add(int32_t i) {
     f.add(q[i]);
     mem += q[i].m_hat;
-    dmin = members.empty() ? q[i].deadline : std::min(dmin, q[i].deadline);
+    if (!expired[i]) {
+      dmin = live ? std::min(dmin, q[i].deadline) : q[i].deadline;
+      live = true;
+    }
     members.push_back(i);
   }
 };
@@ -73,7 +81,8 @@ extern "C" wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *q
       return wisp::report_error(WISP_E_INVALID, "wisp_schedule: request with l_new < 1 or ctx_len < 0");
   *batch_len = 0;
   if (n == 0) return WISP_OK;
-  Batch b{q, *model, t_now, mem_budget};
+  std::vector<char> expired(n, 0);
+  Batch b{q, *model, t_now, mem_budget, expired};
 
   if (policy == WISP_SCHED_FCFS) {
     std::vector<int32_t> order(n);
@@ -93,6 +102,7 @@ extern "C" wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *q
       const double v = batch_time(*model, solo);
       util[i] = q[i].g_hat / v;
       lst[i] = q[i].deadline - v - guard;
+      expired[i] = t_now + v > q[i].deadline;
       (t_now >= lst[i] ? crit : non).push_back(i);
     }
     std::stable_sort(crit.begin(), crit.end(),
@@ -112,10 +122,6 @@ extern "C" wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *q
         if (!b.feasible_with(i)) break;
         b.add(i);
       }
-    }
-    if (b.members.empty()) {   // nothing feasible: the most urgent request goes alone
-      const int32_t head = crit.empty() ? non.front() : crit.front();
-      if (q[head].m_hat <= mem_budget) b.add(head);
     }
   }
   std::copy(b.members.begin(), b.members.end(), batch);

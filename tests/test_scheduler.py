@@ -68,12 +68,20 @@ def test_memory_budget_ends_the_batch(W):
     assert _both(W, reqs, 0, 2.5, 0, "fcfs") == [1, 2]
 
 
-def test_a_request_past_saving_is_dispatched_alone(W):
-    # t = 2: r1 (v 5, d 6) is critical and late (2 + 5 > 6); r0 (v 6, d 10, latest start 4)
-    # is not critical.  Nothing is feasible, so r1 goes alone.
+def test_a_lost_deadline_no_longer_constrains_the_batch(W):
+    # t = 2: r1 (v 5, d 6) misses its deadline even alone (2 + 5 > 6); r0 (v 6, d 10, latest
+    # start 4) is not critical.  r1 is admitted on memory alone; r0 then fits its own
+    # deadline (2 + 1 + 2 + 4 = 9 <= 10) although the batch ends after r1's deadline.
     reqs = [R(2, 10), R(1, 6)]
+    assert _both(W, reqs, 2, 10.0, 0) == [1, 0]
+    # r0 now has d 12 (latest start 2: critical).  In deadline order r1 comes first, and r0
+    # would end at 2 + 11 = 13 > 12 in its company, although alone it would make 12 <= 12
+    reqs = [R(6, 12), R(1, 6)]
     assert _both(W, reqs, 2, 10.0, 0) == [1]
-    # a request larger than the memory budget is never dispatched
+    # a queue of lost requests goes out in deadline order while memory lasts
+    reqs = [R(3, 5, m=1.0), R(1, 3, m=1.0), R(2, 4, m=1.0), R(1, 100, m=1.0)]
+    assert _both(W, reqs, 2, 2.5, 0) == [1, 2]
+    # a request whose memory alone exceeds the budget is never dispatched
     assert _both(W, [R(1, 100, m=5.0)], 0, 2.0, 0) == []
 
 
@@ -117,13 +125,16 @@ def test_native_scheduler_matches_the_oracle_on_random_queues(W):
         got = W.wisp_schedule(W.WISP_SCHED_SLO, reqs, t, budget, guard, model)
         assert got == ref, trial
         assert W.wisp_schedule(W.WISP_SCHED_FCFS, reqs, t, budget, guard, model) == schedule_fcfs(reqs, budget)
-        # invariants: distinct members within memory; a batch of two or more meets its
-        # tightest deadline under the estimator (a single request may be a late one)
+        # invariants: distinct members within memory; the batch meets the deadline of every
+        # member that could still meet it alone, under the estimator; the queue never stalls
         assert len(set(got)) == len(got)
         assert sum(reqs[i].m_hat for i in got) <= budget
-        if len(got) >= 2:
-            members = [reqs[i] for i in got]
-            assert t + batch_time(model, members) <= min(r.deadline for r in members)
+        members = [reqs[i] for i in got]
+        live = [r.deadline for r in members if t + batch_time(model, [r]) <= r.deadline]
+        if live:
+            assert t + batch_time(model, members) <= min(live)
+        if reqs and all(r.m_hat <= budget for r in reqs):
+            assert got
 
 
 def test_schedule_errors(W):
