@@ -17,6 +17,15 @@ Training set (123):
 Test set (50, never seen by the fit): 10 / 15 / 25 draws of categories 3 / 4 / 5 from a
 different seed.
 
+Serving-range extension (``--design serving``; not part of App. C): App. C's largest batch
+holds 8 follow-ups with at most 32k cached tokens, while this GPU verifies batches of
+hundreds of follow-ups with up to a million cached tokens, where the cached-KV read term
+decides the step time and App. C's design leaves it unidentified.  Category 6 adds 30
+training and 15 test batches of 16 .. 256 follow-ups (L_cached 128 .. 3072, 1 .. 5
+drafts), a third of them with 1 .. 3 first-time verifications (prompts of 100 .. 600
+tokens) mixed in.  ``--replay FILE`` times the batch compositions a simulator run recorded
+(regenerated from its JSON record) and reports the fit's error on them.
+
 Each configuration is timed as App. C does: 10 warm-up steps, then 3 timed steps (HIP
 events on the calling stream); the coefficient of variation of the 3 is recorded.  Inputs
 are synthetic (the KV content and the tokens do not change the step's work).  The fit
@@ -40,6 +49,7 @@ from .latency_model import fit_report, step_features
 
 PAGE = 16
 DRAFTS = 5
+REPLAY_MAX_ROWS = 4096
 
 
 @dataclass
@@ -75,6 +85,16 @@ def _random_configs(rng, cat: int):
         new = rng.integers(1, 21, size=B)
         tot = rng.integers(1000, 4001, size=B)
         return tot - new, new
+    if cat == 6:
+        B = int(rng.choice([16, 32, 64, 128, 192, 256]))
+        ctx = rng.integers(128, 3073, size=B)
+        new = rng.integers(2, 7, size=B)
+        if rng.random() < 1 / 3:
+            k = int(rng.integers(1, 4))
+            ctx[:k] = 0
+            new[:k] = rng.integers(100, 601, size=k) + 1 + DRAFTS
+        perm = rng.permutation(B)
+        return ctx[perm], new[perm]
     n_cold = int(rng.integers(1, 3))
     n_warm = int(rng.integers(2, 9))
     ctx = np.concatenate([np.zeros(n_cold, int), rng.integers(500, 4001, size=n_warm)])
@@ -83,8 +103,9 @@ def _random_configs(rng, cat: int):
     return ctx[perm], new[perm]
 
 
-def sweep_configs(seed: int = 20260111, test_seed: int = 7) -> list:
-    """The 173 configurations (123 training, 50 test), deterministic in the seeds."""
+def sweep_configs(seed: int = 20260111, test_seed: int = 7, serving: bool = False) -> list:
+    """The 173 configurations (123 training, 50 test), deterministic in the seeds; with
+    `serving`, followed by the 45 of the serving-range extension (30 training, 15 test)."""
     out = []
 
     def add(cat, split, ctx, new):
@@ -107,6 +128,11 @@ def sweep_configs(seed: int = 20260111, test_seed: int = 7) -> list:
     for cat, n in ((3, 10), (4, 15), (5, 25)):
         for _ in range(n):
             add(cat, "test", *_random_configs(rng, cat))
+    if serving:
+        for split, s, n in (("train", seed + 6, 30), ("test", test_seed + 6, 15)):
+            rng = np.random.default_rng(s)
+            for _ in range(n):
+                add(6, split, *_random_configs(rng, 6))
     return out
 
 
@@ -194,29 +220,77 @@ def fit(rows, configs) -> dict:
     return rep
 
 
+def replay(path: str, shape, log=print) -> dict:
+    """Time the batch compositions a simulator run recorded and compare them with the
+    estimator that run used (the error of its batch-time model in its own regime)."""
+    from .slo_sim import replay_batches
+    src = json.load(open(path))
+    a, bc, br, c = src["model"]
+    batches = replay_batches(src)
+    # batches beyond the sizes the verification path is tested at (REPLAY_MAX_ROWS rows) stay out
+    kept = [b for b in batches if sum(b["l_new"]) <= REPLAY_MAX_ROWS]
+    configs = [SweepConfig(k, 0, "replay", b["ctx_len"], b["l_new"]) for k, b in enumerate(kept)]
+    rows = measure(configs, shape, log=log)
+    meas = np.array([r["ms_mean"] / 1e3 for r in rows])
+    pred = np.array([a * r["N_linear"] + bc * r["N_interactions"] + br * r["N_cached"] + c for r in rows])
+    rel = (pred - meas) / meas
+    return {"source": path, "model": src["model"], "rows": rows, "n": len(rows),
+            "skipped_over_max_rows": len(batches) - len(kept),
+            "mape_pct": float(100 * np.abs(rel).mean()), "mean_rel_err_pct": float(100 * rel.mean()),
+            "p90_abs_rel_err_pct": float(100 * np.quantile(np.abs(rel), 0.9)),
+            "ms_range": [float(1e3 * meas.min()), float(1e3 * meas.max())]}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--out", default="profiles/latency_model_8b.json")
     ap.add_argument("--model", default="8b", choices=("8b", "70b"))
+    ap.add_argument("--design", default="appc", choices=("appc", "serving"),
+                    help="App. C's 173 configurations, or those plus the serving-range extension")
+    ap.add_argument("--replay", default="", help="time the batches recorded in a simulator JSON record")
     ap.add_argument("--limit", type=int, default=0, help="time only the first N configurations")
     args = ap.parse_args(argv)
     import wisp_inputs as wi
     shape = wi.LLAMA3_8B if args.model == "8b" else wi.LLAMA3_70B
-    configs = sweep_configs()
+    t0 = time.time()
+    if args.replay:
+        rec = replay(args.replay, shape, log=lambda m: print(m, flush=True))
+        rec["seconds"] = time.time() - t0
+        with open(args.out, "w") as f:
+            json.dump(rec, f, indent=1)
+        print(json.dumps({k: rec[k] for k in ("n", "mape_pct", "mean_rel_err_pct", "p90_abs_rel_err_pct",
+                                               "ms_range")}), flush=True)
+        return
+    configs = sweep_configs(serving=args.design == "serving")
     if args.limit:
         configs = configs[:args.limit]
-    t0 = time.time()
     rows = measure(configs, shape, log=lambda m: print(m, flush=True))
-    rep = fit(rows, configs)
+    appc = [c for c in configs if c.category <= 5]
+    rep = fit(rows, appc)
     rec = {"model": shape.name, "protocol": "10 warm-up + 3 timed steps per configuration (App. C)",
            "fit": rep, "rows": rows, "seconds": time.time() - t0}
+    summary = {"a": rep["model"]["a"], "b_compute": rep["model"]["b_compute"], "b_read": rep["model"]["b_read"],
+               "c": rep["model"]["c"], "train_r2": rep["train"]["r2"], "test_r2": rep["test"]["r2"],
+               "test_mape_pct": rep["test"]["mape_pct"]}
+    if args.design == "serving":
+        srv = fit(rows, configs)
+        rec["fit_serving"] = srv
+        # the App. C fit's error on the serving-range batches it never saw
+        six = [r for r in rows if r["category"] == 6]
+        m = rep["model"]
+        pred = np.array([m["a"] * r["N_linear"] + m["b_compute"] * r["N_interactions"] + m["b_read"] * r["N_cached"]
+                         + m["c"] for r in six])
+        meas = np.array([r["ms_mean"] / 1e3 for r in six])
+        rec["appc_fit_on_serving_range"] = {"mape_pct": float(100 * np.mean(np.abs(pred - meas) / meas)),
+                                            "mean_rel_err_pct": float(100 * np.mean((pred - meas) / meas))}
+        summary["serving"] = {k: srv["model"][k] for k in ("a", "b_compute", "b_read", "c")}
+        summary["serving"].update(train_r2=srv["train"]["r2"], test_r2=srv["test"]["r2"],
+                                  test_mape_pct=srv["test"]["mape_pct"])
+        summary["appc_fit_on_serving_range"] = rec["appc_fit_on_serving_range"]
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     with open(args.out, "w") as f:
         json.dump(rec, f, indent=1)
-    m = rep["model"]
-    print(json.dumps({"a": m["a"], "b_compute": m["b_compute"], "b_read": m["b_read"], "c": m["c"],
-                      "train_r2": rep["train"]["r2"], "test_r2": rep["test"]["r2"],
-                      "test_mape_pct": rep["test"]["mape_pct"]}), flush=True)
+    print(json.dumps(summary), flush=True)
 
 
 if __name__ == "__main__":

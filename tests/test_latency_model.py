@@ -98,3 +98,27 @@ def test_sweep_configurations():
     # a cold start's interactions are quadratic in its new tokens
     cold = ls.step_features([0], [5], [94])
     assert cold[0] == 100 and cold[1] == 100 * 100 and cold[2] == 0
+
+
+def test_serving_range_extension():
+    """The serving-range extension appends 30 training and 15 test batches of 16 .. 256
+    follow-ups (cache 128 .. 3072, 1 .. 5 drafts), some with 1 .. 3 first-time verifications
+    mixed in, and leaves App. C's 173 configurations untouched."""
+    from paper_2601_11652_amd import latency_sweep as ls
+    base = ls.sweep_configs()
+    ext = ls.sweep_configs(serving=True)
+    assert [(c.ctx_len, c.l_new, c.split) for c in ext[:173]] == [(c.ctx_len, c.l_new, c.split) for c in base]
+    six = ext[173:]
+    assert len(six) == 45 and all(c.category == 6 for c in six)
+    assert sum(c.split == "train" for c in six) == 30 and sum(c.split == "test" for c in six) == 15
+    n_cold = 0
+    for c in six:
+        assert c.B in (16, 32, 64, 128, 192, 256)
+        for ctx, g, pre, n in zip(c.ctx_len, c.gamma, c.prefill_len, c.l_new):
+            if ctx == 0:
+                n_cold += 1
+                assert g == 5 and 100 <= pre <= 600
+            else:
+                assert 128 <= ctx <= 3072 and 1 <= g <= 5 and pre == 0
+    assert n_cold > 0
+    assert max(sum(c.l_new) for c in six) <= ls.REPLAY_MAX_ROWS
