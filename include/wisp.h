@@ -274,6 +274,55 @@ wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *requests, in
                           double mem_budget, double guard, const wisp_latency_model *model,
                           int32_t *batch, int32_t *batch_len);
 
+/*
+ * KV page-pool manager for multi-round sessions (Sec. 4.5: each round forwards only the
+ * newly drafted block and updates the session's KV in place, the committed prefix staying
+ * cached across rounds), host code.  It hands out the page ids that the page tables of
+ * wisp_batch_desc hold; the pool memory itself (wisp_kv) belongs to the caller.  Not
+ * thread-safe: one manager per thread, or external locking.
+ *
+ * Sessions are caller-chosen int64 ids.  Pages are given out lowest id first.
+ *   wisp_kvm_lookup   cached[i] = tokens whose KV is held for sid[i]; 0 for a session the
+ *                     manager does not hold (new, released or evicted), whose owner must
+ *                     then send its whole sequence as prefill (ctx_len = 0).
+ *   wisp_kvm_reserve  makes each sid[i] (created if new) hold pages for n_tokens[i]
+ *                     positions, n_tokens[i] >= its cached tokens (a round reserves
+ *                     ctx_len + prefill_len + gamma + 1), and writes its page ids to
+ *                     page_table[i * pt_stride ..], -1 past its last page.  When the free
+ *                     pages do not suffice, sessions outside the call are evicted least
+ *                     recently used first (ties: smaller id).  On WISP_E_CAPACITY (the
+ *                     pool cannot hold the call even after evicting every other session,
+ *                     or a row of pt_stride is too short) nothing changes.  *n_evicted
+ *                     (may be NULL) = sessions this call evicted.
+ *   wisp_kvm_commit   rollback by length: sid[i] keeps the KV of its first cached[i]
+ *                     tokens (at most the positions reserved); whole pages past them
+ *                     return to the pool.  A round commits ctx_len + prefill_len + L + 1
+ *                     (prompt rows, root and accepted drafts; the extra token is the next
+ *                     round's root).  Commit a round before reserving the next batch: a
+ *                     session evicted in between cannot be committed (WISP_E_INVALID).
+ *   wisp_kvm_release  forgets the sessions and frees their pages (unknown ids ignored).
+ * reserve and commit mark their sessions as used (one clock tick per call).  Errors:
+ * WISP_E_INVALID for NULL pointers, n < 0, a session twice in one call, n_tokens below
+ * the cached tokens, or a commit outside the reserved pages.
+ */
+typedef struct wisp_kv_manager wisp_kv_manager;
+
+typedef struct {
+  int32_t n_pages, free_pages, sessions;       /* pool size, free pages, resident sessions  */
+  int64_t evictions, pages_evicted;            /* sessions evicted, their pages              */
+  int64_t pages_allocated, pages_freed;        /* by reserve; by commit and release          */
+  int64_t lookup_hits, lookup_misses;          /* lookups that found cached tokens, or none  */
+} wisp_kvm_stats;
+
+wisp_status wisp_kvm_create(int32_t n_pages, int32_t page_size, wisp_kv_manager **out);
+void wisp_kvm_destroy(wisp_kv_manager *m);
+wisp_status wisp_kvm_lookup(wisp_kv_manager *m, const int64_t *sid, int32_t n, int32_t *cached);
+wisp_status wisp_kvm_reserve(wisp_kv_manager *m, const int64_t *sid, const int32_t *n_tokens, int32_t n,
+                             int32_t *page_table, int32_t pt_stride, int32_t *n_evicted);
+wisp_status wisp_kvm_commit(wisp_kv_manager *m, const int64_t *sid, const int32_t *cached, int32_t n);
+wisp_status wisp_kvm_release(wisp_kv_manager *m, const int64_t *sid, int32_t n);
+wisp_status wisp_kvm_get_stats(const wisp_kv_manager *m, wisp_kvm_stats *out);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char *wisp_last_error(void);
 

@@ -7,7 +7,8 @@ the library has not been built -- there is no fallback implementation.
 
 Entry points keep the C names: wisp_verify, wisp_accept, wisp_attention,
 wisp_pack_linear, wisp_workspace_size, wisp_accept_workspace_size, wisp_uniform,
-wisp_check, wisp_last_error, wisp_schedule.  ``GpuModel`` and ``BatchDesc`` assemble the C structs.
+wisp_check, wisp_last_error, wisp_schedule; ``KVManager`` wraps the wisp_kvm_* calls.
+``GpuModel`` and ``BatchDesc`` assemble the C structs.
 """
 from __future__ import annotations
 
@@ -35,7 +36,9 @@ TAG_RACE = 2
 
 EXPORTS = ("wisp_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
            "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
-           "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule")
+           "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule", "wisp_kvm_create",
+           "wisp_kvm_destroy", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit", "wisp_kvm_release",
+           "wisp_kvm_get_stats")
 
 
 class WispError(RuntimeError):
@@ -74,6 +77,12 @@ class wisp_latency_model(C.Structure):
 class wisp_sched_request(C.Structure):
     _fields_ = [("arrival", C.c_double), ("deadline", C.c_double), ("g_hat", C.c_double),
                 ("m_hat", C.c_double), ("ctx_len", C.c_int32), ("l_new", C.c_int32)]
+
+
+class wisp_kvm_stats(C.Structure):
+    _fields_ = [("n_pages", C.c_int32), ("free_pages", C.c_int32), ("sessions", C.c_int32),
+                ("evictions", C.c_int64), ("pages_evicted", C.c_int64), ("pages_allocated", C.c_int64),
+                ("pages_freed", C.c_int64), ("lookup_hits", C.c_int64), ("lookup_misses", C.c_int64)]
 
 
 WISP_SCHED_SLO = 0
@@ -117,9 +126,19 @@ def _load():
     L.wisp_schedule.argtypes = [C.c_int32, C.POINTER(wisp_sched_request), C.c_int32, C.c_double, C.c_double,
                                 C.c_double, C.POINTER(wisp_latency_model), C.POINTER(C.c_int32),
                                 C.POINTER(C.c_int32)]
+    _I32P, _I64P = C.POINTER(C.c_int32), C.POINTER(C.c_int64)
+    L.wisp_kvm_create.argtypes = [C.c_int32, C.c_int32, C.POINTER(_VP)]
+    L.wisp_kvm_destroy.argtypes = [_VP]
+    L.wisp_kvm_destroy.restype = None
+    L.wisp_kvm_lookup.argtypes = [_VP, _I64P, C.c_int32, _I32P]
+    L.wisp_kvm_reserve.argtypes = [_VP, _I64P, _I32P, C.c_int32, _I32P, C.c_int32, _I32P]
+    L.wisp_kvm_commit.argtypes = [_VP, _I64P, _I32P, C.c_int32]
+    L.wisp_kvm_release.argtypes = [_VP, _I64P, C.c_int32]
+    L.wisp_kvm_get_stats.argtypes = [_VP, C.POINTER(wisp_kvm_stats)]
     for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
                  "wisp_check", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
-                 "wisp_schedule"):
+                 "wisp_schedule", "wisp_kvm_create", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit",
+                 "wisp_kvm_release", "wisp_kvm_get_stats"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -338,6 +357,69 @@ def wisp_schedule(policy: int, requests, t_now: float, mem_budget: float, guard:
     m = wisp_latency_model(*[float(x) for x in model])
     _ok(lib.wisp_schedule(policy, arr, n, t_now, mem_budget, guard, C.byref(m), out, C.byref(k)))
     return list(out[:k.value])
+
+
+class KVManager:
+    """A wisp_kv_manager (host code): page ids for multi-round sessions over a pool of
+    n_pages pages (Sec. 4.5's in-place, prefix-cached KV).  Arrays are numpy."""
+
+    def __init__(self, n_pages: int, page_size: int = PAGE):
+        h = _VP()
+        _ok(lib.wisp_kvm_create(n_pages, page_size, C.byref(h)))
+        self._h = h
+        self.page_size = page_size
+
+    @staticmethod
+    def _ids(sids):
+        a = np.ascontiguousarray(sids, dtype=np.int64)
+        return a, a.ctypes.data_as(C.POINTER(C.c_int64))
+
+    @staticmethod
+    def _i32(x, n):
+        a = np.ascontiguousarray(np.broadcast_to(np.asarray(x, dtype=np.int32), (n,)))
+        return a, a.ctypes.data_as(C.POINTER(C.c_int32))
+
+    def lookup(self, sids) -> np.ndarray:
+        ids, pid = self._ids(sids)
+        out = np.zeros(ids.shape[0], np.int32)
+        _ok(lib.wisp_kvm_lookup(self._h, pid, ids.shape[0], out.ctypes.data_as(C.POINTER(C.c_int32))))
+        return out
+
+    def reserve(self, sids, n_tokens, pt_stride: int):
+        """(page table [n][pt_stride] int32, sessions evicted by the call)."""
+        ids, pid = self._ids(sids)
+        n = ids.shape[0]
+        nt, pnt = self._i32(n_tokens, n)
+        table = np.full((n, pt_stride), -1, np.int32)
+        ev = C.c_int32(0)
+        _ok(lib.wisp_kvm_reserve(self._h, pid, pnt, n, table.ctypes.data_as(C.POINTER(C.c_int32)), pt_stride,
+                                 C.byref(ev)))
+        return table, ev.value
+
+    def commit(self, sids, cached):
+        ids, pid = self._ids(sids)
+        c, pc = self._i32(cached, ids.shape[0])
+        _ok(lib.wisp_kvm_commit(self._h, pid, pc, ids.shape[0]))
+
+    def release(self, sids):
+        ids, pid = self._ids(sids)
+        _ok(lib.wisp_kvm_release(self._h, pid, ids.shape[0]))
+
+    def stats(self) -> dict:
+        st = wisp_kvm_stats()
+        _ok(lib.wisp_kvm_get_stats(self._h, C.byref(st)))
+        return {k: getattr(st, k) for k, _ in wisp_kvm_stats._fields_}
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib.wisp_kvm_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def wisp_check(workspace, stream=None):
