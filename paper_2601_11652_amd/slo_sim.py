@@ -1,4 +1,4 @@
-"""Verification-workload simulator for the SLO-aware batch scheduler (Sec. 3, Sec. 4.3, Sec. 5).
+"""Verification-workload simulator for the SLO-aware batch scheduler (Sec. 3.1, Sec. 4.3, Sec. 5).
 
 N edge devices iterate speculate -> verify against one verification GPU.  Device k has a
 token-speed class s_k in {2, 4, 6, 8} tok/s (classes 1 .. 4, assigned round-robin), an
@@ -13,7 +13,7 @@ gamma_k tokens, sends them, and gets back L + 1 committed tokens, where the numb
 accepted drafts follows the speculative-sampling law at rate alpha_k (P(L >= j) = alpha^j,
 j <= gamma).
 
-Each verification request carries the server-side budget of Sec. 3,
+Each verification request carries the server-side budget of Sec. 3.1,
 tau = alpha * N_d / s_c - T_draft - T_network, as its relative deadline, the expected
 verified tokens g = alpha * N_d as its value, and as its memory footprint its new rows
 (its cached prefix is resident already; what a verification adds is KV and activations for
