@@ -323,6 +323,44 @@ wisp_status wisp_kvm_commit(wisp_kv_manager *m, const int64_t *sid, const int32_
 wisp_status wisp_kvm_release(wisp_kv_manager *m, const int64_t *sid, int32_t n);
 wisp_status wisp_kvm_get_stats(const wisp_kv_manager *m, wisp_kvm_stats *out);
 
+/*
+ * Draft-side rejection predictor (Sec. 3.3, Sec. 4.1, App. B): statistics of the draft
+ * model's next-token distribution, and the MLP (hidden widths 512, 128, 64) that turns
+ * them into the probability that the drafted token is accepted; the drafting controller
+ * stops drafting at the first predicted rejection.
+ *
+ * wisp_draft_stats: for each of `rows` rows of DEVICE fp32 logits (row r at logits + r*ld,
+ *   `vocab` finite entries, ld >= vocab), with z = logits / temperature and p = softmax(z),
+ *   writes DEVICE fp32 stats[r][4] = (confidence max_k p_k, entropy -sum p ln p (nats),
+ *   top-2 margin p_(1) - p_(2) (0 when the maximum repeats, p_(1) when vocab = 1),
+ *   dispersion: the population standard deviation of z).  stats and workspace (DEVICE,
+ *   wisp_draft_stats_workspace_size bytes: per-chunk partial sums) must be 16-byte aligned.
+ * wisp_reject_predict: for each of `rows` feature rows (DEVICE fp32 [rows][n_in]), with
+ *   x = (f - mean) * inv_std, writes DEVICE fp32 p_accept[r] =
+ *   sigmoid(w4 . relu(W3 relu(W2 relu(W1 x + b1) + b2) + b3) + b4).  The features are the
+ *   four statistics above, optionally followed by caller-chosen ones (the draft position,
+ *   say); all weights are DEVICE fp32, row-major [out][in], w2 16-byte and w3 8-byte
+ *   aligned.  At most 65535 rows per wisp_draft_stats call (WISP_E_UNSUPPORTED beyond).
+ * Errors: WISP_E_INVALID for NULL pointers, rows < 0, vocab < 1, ld < vocab,
+ * temperature <= 0 or n_in outside 1..8; WISP_E_WORKSPACE for a short workspace.  Both only
+ * enqueue work on `stream`.
+ */
+typedef struct {
+  int32_t n_in;                  /* features per row, 1..8                                 */
+  const float *mean, *inv_std;   /* DEVICE [n_in] input standardisation                    */
+  const float *w1, *b1;          /* DEVICE [512][n_in], [512]                              */
+  const float *w2, *b2;          /* DEVICE [128][512], [128]                               */
+  const float *w3, *b3;          /* DEVICE [64][128], [64]                                 */
+  const float *w4;               /* DEVICE [64]                                            */
+  float b4;
+} wisp_reject_mlp;
+
+size_t wisp_draft_stats_workspace_size(int32_t rows, int32_t vocab);
+wisp_status wisp_draft_stats(const float *logits, int32_t rows, int32_t vocab, int64_t ld, float temperature,
+                             float *stats, void *workspace, size_t workspace_bytes, void *stream);
+wisp_status wisp_reject_predict(const wisp_reject_mlp *mlp, const float *features, int32_t rows, float *p_accept,
+                                void *stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char *wisp_last_error(void);
 

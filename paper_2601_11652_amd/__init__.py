@@ -7,7 +7,8 @@ the library has not been built -- there is no fallback implementation.
 
 Entry points keep the C names: wisp_verify, wisp_accept, wisp_attention,
 wisp_pack_linear, wisp_workspace_size, wisp_accept_workspace_size, wisp_uniform,
-wisp_check, wisp_last_error, wisp_schedule; ``KVManager`` wraps the wisp_kvm_* calls.
+wisp_check, wisp_last_error, wisp_schedule, wisp_draft_stats, wisp_reject_predict;
+``KVManager`` wraps the wisp_kvm_* calls and ``RejectMLP`` the predictor's weights.
 ``GpuModel`` and ``BatchDesc`` assemble the C structs.
 """
 from __future__ import annotations
@@ -38,7 +39,7 @@ EXPORTS = ("wisp_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linea
            "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
            "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule", "wisp_kvm_create",
            "wisp_kvm_destroy", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit", "wisp_kvm_release",
-           "wisp_kvm_get_stats")
+           "wisp_kvm_get_stats", "wisp_draft_stats_workspace_size", "wisp_draft_stats", "wisp_reject_predict")
 
 
 class WispError(RuntimeError):
@@ -83,6 +84,12 @@ class wisp_kvm_stats(C.Structure):
     _fields_ = [("n_pages", C.c_int32), ("free_pages", C.c_int32), ("sessions", C.c_int32),
                 ("evictions", C.c_int64), ("pages_evicted", C.c_int64), ("pages_allocated", C.c_int64),
                 ("pages_freed", C.c_int64), ("lookup_hits", C.c_int64), ("lookup_misses", C.c_int64)]
+
+
+class wisp_reject_mlp(C.Structure):
+    _fields_ = [("n_in", C.c_int32), ("mean", C.c_void_p), ("inv_std", C.c_void_p), ("w1", C.c_void_p),
+                ("b1", C.c_void_p), ("w2", C.c_void_p), ("b2", C.c_void_p), ("w3", C.c_void_p),
+                ("b3", C.c_void_p), ("w4", C.c_void_p), ("b4", C.c_float)]
 
 
 WISP_SCHED_SLO = 0
@@ -135,10 +142,14 @@ def _load():
     L.wisp_kvm_commit.argtypes = [_VP, _I64P, _I32P, C.c_int32]
     L.wisp_kvm_release.argtypes = [_VP, _I64P, C.c_int32]
     L.wisp_kvm_get_stats.argtypes = [_VP, C.POINTER(wisp_kvm_stats)]
+    L.wisp_draft_stats_workspace_size.argtypes = [C.c_int32, C.c_int32]
+    L.wisp_draft_stats_workspace_size.restype = C.c_size_t
+    L.wisp_draft_stats.argtypes = [_VP, C.c_int32, C.c_int32, C.c_int64, C.c_float, _VP, _VP, C.c_size_t, _VP]
+    L.wisp_reject_predict.argtypes = [C.POINTER(wisp_reject_mlp), _VP, C.c_int32, _VP, _VP]
     for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
                  "wisp_check", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
                  "wisp_schedule", "wisp_kvm_create", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit",
-                 "wisp_kvm_release", "wisp_kvm_get_stats"):
+                 "wisp_kvm_release", "wisp_kvm_get_stats", "wisp_draft_stats", "wisp_reject_predict"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -357,6 +368,34 @@ def wisp_schedule(policy: int, requests, t_now: float, mem_budget: float, guard:
     m = wisp_latency_model(*[float(x) for x in model])
     _ok(lib.wisp_schedule(policy, arr, n, t_now, mem_budget, guard, C.byref(m), out, C.byref(k)))
     return list(out[:k.value])
+
+
+def wisp_draft_stats(logits, vocab: int, temperature: float, stats, ws=None, stream=None):
+    """stats [rows][4] fp32 (confidence, entropy, top-2 margin, std of z) of logits rows
+    [rows][ld] fp32 (the first `vocab` entries of each row), z = logits / temperature.
+    `ws` (a device byte tensor of wisp_draft_stats_workspace_size bytes) is allocated when
+    not given."""
+    rows = logits.shape[0]
+    if ws is None:
+        ws = workspace(lib.wisp_draft_stats_workspace_size(rows, vocab))
+    _ok(lib.wisp_draft_stats(_ptr(logits), rows, vocab, logits.stride(0), temperature, _ptr(stats), _ptr(ws),
+                             ws.numel(), _stream(stream)))
+
+
+class RejectMLP:
+    """Device weights of the rejection predictor MLP (hidden 512, 128, 64; fp32 tensors
+    w1 [512][n_in], b1, w2 [128][512], b2, w3 [64][128], b3, w4 [64], scalar b4, and the input
+    standardisation mean / inv_std [n_in])."""
+
+    def __init__(self, params: dict):
+        self.t = {k: v.contiguous() for k, v in params.items() if k != "b4"}
+        self.c = wisp_reject_mlp(int(self.t["w1"].shape[1]), *[self.t[k].data_ptr() for k in
+                                 ("mean", "inv_std", "w1", "b1", "w2", "b2", "w3", "b3", "w4")], float(params["b4"]))
+
+
+def wisp_reject_predict(mlp: RejectMLP, features, p_accept, stream=None):
+    _ok(lib.wisp_reject_predict(C.byref(mlp.c), _ptr(features), features.shape[0], _ptr(p_accept),
+                                _stream(stream)))
 
 
 class KVManager:
