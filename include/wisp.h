@@ -123,8 +123,10 @@ typedef struct {
                                     before the root; NULL = none                            */
 } wisp_batch_desc;
 
-/* Bytes of DEVICE workspace wisp_verify needs for this model and batch (0 on error). */
+/* Bytes of DEVICE workspace wisp_verify needs for this model and batch (0 on error), and
+ * the extra bytes it needs when the caller passes no target_logits buffer. */
 size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc);
+size_t wisp_logits_workspace_size(const wisp_model *model, const wisp_batch_desc *desc);
 
 /*
  * Pack one linear weight (natural [rows][cols] row-major, DEVICE `src`) into the
@@ -152,7 +154,9 @@ wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t c
  *   accept_len    DEVICE int32 [B]: L_i = R_i - 1 (Eq. (2))
  *   out_tokens    DEVICE int32 [M]: request i's slots hold y_1..y_L, the extra token, then -1
  *   target_logits DEVICE fp32 [M][vocab]: the target's logits of every verification row
- *                 (root .. y_gamma of each request; prompt rows produce none) (required)
+ *                 (root .. y_gamma of each request; prompt rows produce none), or NULL: the
+ *                 logits then live in the workspace, which must hold
+ *                 wisp_workspace_size + wisp_logits_workspace_size bytes
  *   workspace     DEVICE scratch of >= wisp_workspace_size() bytes
  * KV: K/V of all prefill_len+gamma+1 new positions are written in place (rejected
  * drafts included); the valid prefix afterwards is ctx_len + prefill_len + 1 + L and

@@ -35,7 +35,7 @@ GAMMA_MAX = 16
 TAG_ACCEPT = 1
 TAG_RACE = 2
 
-EXPORTS = ("wisp_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
+EXPORTS = ("wisp_workspace_size", "wisp_logits_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
            "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
            "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule", "wisp_kvm_create",
            "wisp_kvm_destroy", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit", "wisp_kvm_release",
@@ -113,6 +113,8 @@ def _load():
     L = C.CDLL(LIB_PATH)
     L.wisp_workspace_size.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_batch_desc)]
     L.wisp_workspace_size.restype = C.c_size_t
+    L.wisp_logits_workspace_size.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_batch_desc)]
+    L.wisp_logits_workspace_size.restype = C.c_size_t
     L.wisp_accept_workspace_size.argtypes = [C.POINTER(wisp_batch_desc), C.c_int32]
     L.wisp_accept_workspace_size.restype = C.c_size_t
     L.wisp_pack_linear.argtypes = [_VP, _VP, C.c_int32, C.c_int32, C.c_int32, _VP]
@@ -322,6 +324,11 @@ class GpuModel:
 # ------------------------------------------------------------------------------------------
 def wisp_workspace_size(model: wisp_model, desc: BatchDesc) -> int:
     return int(lib.wisp_workspace_size(C.byref(model), C.byref(desc.c)))
+
+
+def wisp_logits_workspace_size(model: wisp_model, desc: BatchDesc) -> int:
+    """Extra workspace bytes wisp_verify needs when target_logits is None."""
+    return int(lib.wisp_logits_workspace_size(C.byref(model), C.byref(desc.c)))
 
 
 def wisp_accept_workspace_size(desc: BatchDesc, vocab: int) -> int:

@@ -571,6 +571,13 @@ size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc)
   return p.total;
 }
 
+size_t wisp_logits_workspace_size(const wisp_model *model, const wisp_batch_desc *desc) {
+  if (check_model(model, false) != WISP_OK || check_desc(desc, false) != WISP_OK) return 0;
+  Plan p;
+  make_plan(p, model, desc, true);
+  return align256((size_t)p.Mv * (size_t)p.V * sizeof(float));
+}
+
 size_t wisp_accept_workspace_size(const wisp_batch_desc *desc, int32_t vocab) {
   if (check_desc(desc, false) != WISP_OK || vocab <= 0) return 0;
   Plan p;
@@ -606,16 +613,19 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
   if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
   if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
   if (kv->n_blocks <= 0) return fail(WISP_E_INVALID, "n_blocks must be positive");
-  if (!tokens || !accept_len || !out_tokens || !target_logits || !workspace)
+  if (!tokens || !accept_len || !out_tokens || !workspace)
     return fail(WISP_E_INVALID, "NULL tokens / outputs / workspace");
   Plan p;
   make_plan(p, model, desc, true);
   if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
   if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
-  if (workspace_bytes < p.total)
-    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
+  // without a caller buffer the logits live in the workspace, after everything else
+  const size_t need = p.total + (target_logits ? 0 : align256((size_t)p.Mv * (size_t)p.V * sizeof(float)));
+  if (workspace_bytes < need)
+    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
   hipStream_t s = (hipStream_t)stream;
   char *ws = (char *)workspace;
+  if (!target_logits) target_logits = reinterpret_cast<float *>(ws + p.total);
   if ((st = upload(p, ws, s)) != WISP_OK) return st;
   StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
   clear_ints(sd.err, 1, s);

@@ -112,3 +112,18 @@ def test_workspace_size_and_pack_validation(W):
     assert L.wisp_pack_linear(FAKE, FAKE, 32, 8, W.WISP_BF16, None) == W.WISP_E_UNSUPPORTED
     assert L.wisp_pack_linear(None, FAKE, 32, 16, W.WISP_BF16, None) == W.WISP_E_INVALID
     assert L.wisp_pack_linear(FAKE, FAKE, 32, 16, 7, None) == W.WISP_E_UNSUPPORTED
+
+
+def test_logits_in_workspace_sizes(W):
+    """Without a target_logits buffer, wisp_verify keeps the logits (verification rows x
+    vocab fp32, 256-byte aligned) after its own workspace and asks for both."""
+    m = _model(W)
+    d = _desc(W, [10, 0], [2, 4], prefill=[0, 30])
+    rows = (2 + 1) + (4 + 1)                            # prompt rows produce no logits
+    assert W.wisp_logits_workspace_size(m, d) == -(-rows * 1024 * 4 // 256) * 256
+    base = W.wisp_workspace_size(m, d)
+    L = W.load_library()
+    kv = W.wisp_kv(FAKE, FAKE, 100, 16)
+    args = (C.byref(m), C.byref(kv), C.byref(d.c), FAKE, FAKE, 1, FAKE, FAKE, None, FAKE)
+    assert L.wisp_verify(*args, base, None) == W.WISP_E_WORKSPACE
+    assert L.wisp_verify(*args, base + W.wisp_logits_workspace_size(m, d) - 1, None) == W.WISP_E_WORKSPACE

@@ -169,3 +169,24 @@ def test_out_of_range_block_id_is_reported():
     good = W.BatchDesc(mix.ctx_len, mix.gamma, to_dev(pt_np), 1.0)
     W.wisp_verify(gm.c, kv, good, tokens, q, 3, acc, out, logits, ws)
     W.wisp_check(ws)
+
+
+def test_logits_kept_in_the_workspace():
+    """target_logits = NULL: the logits live in the caller's workspace and every output is
+    the same as with a logits buffer."""
+    from gpu_harness import Workload, gpu_model, run_gpu, to_dev
+    import oracle
+    from oracle import fixtures as fx
+    mix = wi.make_mix("tiny")
+    wl = Workload(mix, fx.host_model(mix.shape))
+    gm = gpu_model(mix.shape)
+    acc_a, out_a, _, _ = run_gpu(gm, wl)
+    kv = W.KVPool(to_dev(wl.pools0[0]), to_dev(wl.pools0[1]))
+    desc = W.BatchDesc(mix.ctx_len, mix.gamma, to_dev(wl.pt), wl.T, mix.req_id)
+    ws = W.workspace(W.wisp_workspace_size(gm.c, desc) + W.wisp_logits_workspace_size(gm.c, desc))
+    acc = torch.full((mix.B,), -7, dtype=torch.int32, device="cuda")
+    out = torch.full((mix.M,), -7, dtype=torch.int32, device="cuda")
+    W.wisp_verify(gm.c, kv, desc, to_dev(wl.tokens), to_dev(wl.q), wl.seed, acc, out, None, ws)
+    W.wisp_check(ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(acc.cpu().numpy(), acc_a) and np.array_equal(out.cpu().numpy(), out_a)
