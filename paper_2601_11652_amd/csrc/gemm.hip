@@ -215,8 +215,8 @@ static constexpr int kPairedWavesMinMT = 5;
 // sizes; more blocks for larger batches and prompt rows, each re-streaming the weights,
 // mostly from L2 / MALL while the blocks of a tile run together); wide outputs use 64-column
 // wave tiles (one A fragment feeds two products), narrow ones 32-column tiles with a deeper
-// ring (8 waves per workgroup from kPairedWavesMinMT row fragments on).  K is split so that
-// the rounds of one-workgroup-per-CU are as full as possible.
+// ring (8 waves per workgroup from kPairedWavesMinMT row fragments on).  K is split until
+// one workgroup per CU is in flight (one round).
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
@@ -233,32 +233,11 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   c.bn = c.kind == 2 ? 256 : 128;
   const int R = c.kind == 2 ? 4 : 8;
   const int tiles = ((N + c.bn - 1) / c.bn) * c.rb;
-  // The ring kernels hold one workgroup per CU (LDS and registers), so a launch runs in
-  // rounds of 256 workgroups.  Up to 128 output tiles (the verification step's usual row
-  // counts), K is split as far as one round allows.  Beyond that (large batches, prompt
-  // rows) 1, 2 or 4 splits are weighed by how full the rounds are, busy = workgroups /
-  // (rounds * 256), adding at most two rounds to the unsplit launch; among equals the fewest
-  // splits, since every split adds a pass over fp32 partial sums.  (Measured on the 8B
-  // projections at 171 .. 2700 rows: a partly filled last round costs more than the extra
-  // partial sums and per-workgroup start-up of the split.)  Each split keeps at least 4 ring
-  // depths of K.
+  // workgroups resident at once: the ring kernels hold one workgroup per CU (LDS and
+  // registers), so more than one round of 256 would leave a partial second round
   const int max_wg = 256;
   int splits = 1;
-  if (tiles <= 128) {
-    while (splits < 16 && tiles * splits * 2 <= max_wg && KF / (splits * 2) >= 4 * R) splits *= 2;
-  } else {
-    const long r1 = (tiles + max_wg - 1) / max_wg;
-    double best = -1.0;
-    for (int sp = 1; sp <= 4 && (sp == 1 || KF / sp >= 4 * R); sp *= 2) {
-      const long wg = (long)tiles * sp, rounds = (wg + max_wg - 1) / max_wg;
-      if (rounds > r1 + 2) break;
-      const double busy = (double)wg / (double)(rounds * max_wg);
-      if (busy > best + 1e-9) {
-        best = busy;
-        splits = sp;
-      }
-    }
-  }
+  while (splits < 16 && tiles * splits * 2 <= max_wg && KF / (splits * 2) >= 4 * R) splits *= 2;
   int kps = (KF + splits - 1) / splits;
   kps = (kps + R - 1) / R * R;
   c.splits = (KF + kps - 1) / kps;
