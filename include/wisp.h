@@ -255,6 +255,9 @@ wisp_status wisp_profile_reset(void);
  *                   away.
  *   WISP_SCHED_FCFS requests in increasing arrival time (ties: lower index first) while
  *                   sum m <= mem_budget (the scheduler disabled: no deadline test).
+ *   WISP_SCHED_SLO_LIVE  as WISP_SCHED_SLO, except that a request whose deadline is lost
+ *                   already is not critical: it joins the utility fill (an ablation of
+ *                   the reading above, for comparison).
  * batch receives the chosen request indices in admission order (capacity n), batch_len
  * their count (0 when nothing fits).  Errors: WISP_E_INVALID for NULL pointers, n < 0, an
  * unknown policy or a request with l_new < 1 or ctx_len < 0.
@@ -274,6 +277,7 @@ typedef struct {
 
 #define WISP_SCHED_SLO 0
 #define WISP_SCHED_FCFS 1
+#define WISP_SCHED_SLO_LIVE 2
 wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *requests, int32_t n, double t_now,
                           double mem_budget, double guard, const wisp_latency_model *model,
                           int32_t *batch, int32_t *batch_len);

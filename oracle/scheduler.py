@@ -17,6 +17,8 @@ critical admission also skips the utility fill).  Readings where the paper is si
   * a request whose memory alone exceeds the budget is never admitted (the caller has to
     turn it away);
   * FCFS (the scheduler disabled) takes requests in arrival order while memory fits.
+An ablation of the lost-deadline reading (lost_not_urgent) takes such requests out of the
+critical queue altogether and lets them join the utility fill instead.
 Only tests and the benchmarks' baselines may import this module.
 """
 from __future__ import annotations
@@ -46,20 +48,23 @@ def batch_time(model, reqs) -> float:
     return t + c
 
 
-def schedule_slo(reqs, t_now: float, mem_budget: float, guard: float, model) -> list:
-    """Alg. 1 at dispatch epoch t_now; returns the admitted request indices in order."""
+def schedule_slo(reqs, t_now: float, mem_budget: float, guard: float, model, lost_not_urgent: bool = False) -> list:
+    """Alg. 1 at dispatch epoch t_now; returns the admitted request indices in order.
+    With lost_not_urgent (the ablation), a request whose deadline is lost already is not
+    critical and joins the utility fill."""
     n = len(reqs)
     if n == 0:
         return []
     v = [batch_time(model, [r]) for r in reqs]
     utility = [reqs[i].g_hat / v[i] for i in range(n)]
     lst = [reqs[i].deadline - v[i] - guard for i in range(n)]
-    critical = [i for i in range(n) if t_now >= lst[i]]
-    others = [i for i in range(n) if not t_now >= lst[i]]
+    expired = [t_now + v[i] > reqs[i].deadline for i in range(n)]
+    urgent = [t_now >= lst[i] and not (lost_not_urgent and expired[i]) for i in range(n)]
+    critical = [i for i in range(n) if urgent[i]]
+    others = [i for i in range(n) if not urgent[i]]
     critical.sort(key=lambda i: reqs[i].deadline)          # EDF (stable)
     others.sort(key=lambda i: -utility[i])                  # by decreasing utility (stable)
 
-    expired = [t_now + v[i] > reqs[i].deadline for i in range(n)]
 
     batch: list = []
     mem = 0.0

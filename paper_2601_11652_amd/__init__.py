@@ -94,6 +94,7 @@ class wisp_reject_mlp(C.Structure):
 
 WISP_SCHED_SLO = 0
 WISP_SCHED_FCFS = 1
+WISP_SCHED_SLO_LIVE = 2
 
 _lib = None
 

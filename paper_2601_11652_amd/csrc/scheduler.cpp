@@ -74,7 +74,7 @@ extern "C" wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *q
                                      int32_t *batch, int32_t *batch_len) {
   if (!batch_len || n < 0 || (n > 0 && (!q || !batch)) || !model)
     return wisp::report_error(WISP_E_INVALID, "wisp_schedule: NULL pointer or n < 0");
-  if (policy != WISP_SCHED_SLO && policy != WISP_SCHED_FCFS)
+  if (policy != WISP_SCHED_SLO && policy != WISP_SCHED_FCFS && policy != WISP_SCHED_SLO_LIVE)
     return wisp::report_error(WISP_E_INVALID, "wisp_schedule: unknown policy");
   for (int32_t i = 0; i < n; ++i)
     if (q[i].l_new < 1 || q[i].ctx_len < 0)
@@ -103,7 +103,9 @@ extern "C" wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *q
       util[i] = q[i].g_hat / v;
       lst[i] = q[i].deadline - v - guard;
       expired[i] = t_now + v > q[i].deadline;
-      (t_now >= lst[i] ? crit : non).push_back(i);
+      // WISP_SCHED_SLO_LIVE: a request that can no longer make its deadline is not urgent
+      const bool urgent = t_now >= lst[i] && !(policy == WISP_SCHED_SLO_LIVE && expired[i]);
+      (urgent ? crit : non).push_back(i);
     }
     std::stable_sort(crit.begin(), crit.end(),
                      [&](int32_t x, int32_t y) { return q[x].deadline < q[y].deadline; });

@@ -18,7 +18,7 @@ tau = alpha * N_d / s_c - T_draft - T_network, as its relative deadline, the exp
 verified tokens g = alpha * N_d as its value, and as its memory footprint its new rows
 (its cached prefix is resident already; what a verification adds is KV and activations for
 its new tokens), against a budget of MAX_BATCH_ROWS rows per batch.  Whenever the GPU is idle and requests are pending, the policy under test
-(wisp_schedule: the SLO-aware Alg. 1, or FCFS) picks a batch, which runs for the batch
+(wisp_schedule: the SLO-aware Alg. 1, its lost-deadline ablation, or FCFS) picks a batch, which runs for the batch
 time of a fitted estimator (Sec. 4.4) times a lognormal error of the fit's size.
 
 Reported per class, after a warm-up: the share of responses whose token speed (committed
@@ -44,7 +44,7 @@ import time
 
 import numpy as np
 
-from . import WISP_SCHED_FCFS, WISP_SCHED_SLO, lib, wisp_latency_model, wisp_sched_request, _ok
+from . import WISP_SCHED_FCFS, WISP_SCHED_SLO, WISP_SCHED_SLO_LIVE, lib, wisp_latency_model, wisp_sched_request, _ok
 
 CLASSES = (2.0, 4.0, 6.0, 8.0)
 RESPONSE_TOKENS = 128
@@ -339,7 +339,7 @@ def _fmt_row(name, r):
 
 
 VARIANTS = (("fcfs", WISP_SCHED_FCFS, 0.002), ("slo_guard_2ms", WISP_SCHED_SLO, 0.002),
-            ("slo_guard_50ms", WISP_SCHED_SLO, 0.050))
+            ("slo_guard_50ms", WISP_SCHED_SLO, 0.050), ("slo_live_guard_2ms", WISP_SCHED_SLO_LIVE, 0.002))
 
 
 def report(rec: dict, replay: dict | None = None) -> str:
@@ -426,7 +426,8 @@ def main(argv=None):
     model, err = load_model(args.model_json)
     rec = {"model": list(model), "model_err": err, "model_json": os.path.relpath(args.model_json, root),
            "sim_s": args.sim_s, "eps": args.eps, "response_tokens": RESPONSE_TOKENS,
-           "variants": {name: {"policy": "fcfs" if pol == WISP_SCHED_FCFS else "slo", "guard_s": g}
+           "variants": {name: {"policy": {WISP_SCHED_FCFS: "fcfs", WISP_SCHED_SLO: "slo",
+                                          WISP_SCHED_SLO_LIVE: "slo_lost_not_urgent"}[pol], "guard_s": g}
                         for name, pol, g in VARIANTS},
            "sweep": [], "capacity": {}, "bursty": {}}
     ns = [int(x) for x in args.n.split(",")]

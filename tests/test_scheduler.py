@@ -85,6 +85,19 @@ def test_a_lost_deadline_no_longer_constrains_the_batch(W):
     assert _both(W, [R(1, 100, m=5.0)], 0, 2.0, 0) == []
 
 
+def test_lost_deadlines_out_of_the_critical_queue(W):
+    # the ablation: r1 (lost) is no longer critical; r0 (latest start 2, v 10, d 12) is, and
+    # goes alone: adding r1 by utility would end the batch at 2 + 11 = 13 > 12
+    reqs = [R(6, 12), R(1, 6)]
+    ref = schedule_slo(reqs, 2 * U, 10.0, 0.0, MODEL, lost_not_urgent=True)
+    assert ref == [0]
+    assert W.wisp_schedule(W.WISP_SCHED_SLO_LIVE, reqs, 2 * U, 10.0, 0.0, MODEL) == ref
+    # with nothing critical both readings fill by utility: r1 (1/5) before r0 (1/6)
+    reqs = [R(2, 10), R(1, 6)]
+    assert schedule_slo(reqs, 2 * U, 10.0, 0.0, MODEL, lost_not_urgent=True) == [1, 0]
+    assert W.wisp_schedule(W.WISP_SCHED_SLO_LIVE, reqs, 2 * U, 10.0, 0.0, MODEL) == [1, 0]
+
+
 def test_ties_keep_index_order(W):
     reqs = [R(4, 100, g=1), R(4, 100, g=1), R(4, 100, g=1)]
     assert _both(W, reqs, 0, 10.0, 0) == [0, 1, 2]
@@ -125,16 +138,19 @@ def test_native_scheduler_matches_the_oracle_on_random_queues(W):
         got = W.wisp_schedule(W.WISP_SCHED_SLO, reqs, t, budget, guard, model)
         assert got == ref, trial
         assert W.wisp_schedule(W.WISP_SCHED_FCFS, reqs, t, budget, guard, model) == schedule_fcfs(reqs, budget)
+        live = W.wisp_schedule(W.WISP_SCHED_SLO_LIVE, reqs, t, budget, guard, model)
+        assert live == schedule_slo(reqs, t, budget, guard, model, lost_not_urgent=True), trial
         # invariants: distinct members within memory; the batch meets the deadline of every
         # member that could still meet it alone, under the estimator; the queue never stalls
         assert len(set(got)) == len(got)
         assert sum(reqs[i].m_hat for i in got) <= budget
-        members = [reqs[i] for i in got]
-        live = [r.deadline for r in members if t + batch_time(model, [r]) <= r.deadline]
-        if live:
-            assert t + batch_time(model, members) <= min(live)
-        if reqs and all(r.m_hat <= budget for r in reqs):
-            assert got
+        for batch in (got, live):
+            members = [reqs[i] for i in batch]
+            reach = [r.deadline for r in members if t + batch_time(model, [r]) <= r.deadline]
+            if reach:
+                assert t + batch_time(model, members) <= min(reach)
+            if reqs and all(r.m_hat <= budget for r in reqs):
+                assert batch
 
 
 def test_schedule_errors(W):
