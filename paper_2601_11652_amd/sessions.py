@@ -68,7 +68,8 @@ class Sessions:
         for s in sids:
             self.seq.pop(int(s), None)
 
-    # one wisp_verify call; returns (accept_len, out_tokens, logits) as device tensors
+    # one wisp_verify call; returns (accept_len, out_tokens, logits) as device tensors and the
+    # call's time in ms when time_it
     def _call(self, kv, ctx, gamma, prefill, table, tokens, q, rng_seed, req_id, time_it=False):
         torch = self.torch
         pt = torch.as_tensor(table, device="cuda")
@@ -168,8 +169,8 @@ class Sessions:
                         mlp, threshold = self.controller
                         pa = torch.empty(len(idx), dtype=torch.float32, device="cuda")
                         wisp_reject_predict(mlp, feats, pa)
-                        for r, i in enumerate(pa.tolist()):
-                            if i < threshold:
+                        for r, p_accept in enumerate(pa.tolist()):
+                            if p_accept < threshold:
                                 stopped[idx[r]] = True
         return drafts, qrows
 
