@@ -139,3 +139,104 @@ def fit_report(X_train, y_train, X_test, y_test, n_boot: int = 1000, seed: int =
             "train": metrics(y_train, m.predict(X_train)),
             "test": metrics(y_test, m.predict(X_test)),
             "cv_r2_mean": float(cv.mean()), "cv_r2_std": float(cv.std())}
+
+
+# ---------------------------------------------------------------------------------------
+# Roofline-shaped variant (not in the paper): the projections cost the longer of streaming
+# the weights once (a constant) and their row-proportional work, so
+#     T_hat = max(t_w, a * N_linear) + b_compute * N_interactions + b_read * N_cached + c
+# Fitted by nonlinear least squares; for a given knot (t_w / a) the remaining model is linear,
+# so the fit scans the knot and solves OLS on [max(N_linear, knot), N_int, N_cached, 1].
+# ---------------------------------------------------------------------------------------
+@dataclass
+class RooflineModel:
+    a: float
+    knot: float          # N_linear below which the projections cost a * knot (weight streaming)
+    b_compute: float
+    b_read: float
+    c: float
+
+    def predict(self, X) -> np.ndarray:
+        X = np.atleast_2d(np.asarray(X, np.float64))
+        return (self.a * np.maximum(X[:, 0], self.knot) + self.b_compute * X[:, 1] + self.b_read * X[:, 2]
+                + self.c)
+
+
+def _roofline_design(X, knot):
+    X = np.atleast_2d(np.asarray(X, np.float64))
+    return np.column_stack([np.maximum(X[:, 0], knot), X[:, 1], X[:, 2], np.ones(X.shape[0])])
+
+
+def fit_roofline(X, y, knots=None) -> RooflineModel:
+    """Least squares over the knot (a grid through the observed N_linear values) and, for
+    each knot, the linear coefficients."""
+    X = np.atleast_2d(np.asarray(X, np.float64))
+    y = np.asarray(y, np.float64)
+    if knots is None:
+        lo, hi = max(1.0, X[:, 0].min()), X[:, 0].max()
+        knots = np.unique(np.concatenate([[0.0], np.geomspace(lo, hi, 400)]))
+    best = None
+    for k in knots:
+        w, *_ = np.linalg.lstsq(_roofline_design(X, k), y, rcond=None)
+        sse = float(np.sum((_roofline_design(X, k) @ w - y) ** 2))
+        if best is None or sse < best[0]:
+            best = (sse, k, w)
+    _, k, w = best
+    return RooflineModel(a=float(w[0]), knot=float(k), b_compute=float(w[1]), b_read=float(w[2]), c=float(w[3]))
+
+
+def roofline_report(X_train, y_train, X_test, y_test) -> dict:
+    m = fit_roofline(X_train, y_train)
+    return {"model": asdict(m), "train": metrics(y_train, m.predict(X_train), 4),
+            "test": metrics(y_test, m.predict(X_test), 4)}
+
+
+def compare_on_sweep(sweep: dict, replay: dict | None = None) -> dict:
+    """The linear estimator and the roofline-shaped variant fitted on the same measured
+    sweep (App. C configurations, and those plus the serving range), scored on the held-out
+    configurations and, if given, on replayed simulator batches."""
+    rows = sweep["rows"]
+
+    def xy(sel):
+        X = np.array([[r["N_linear"], r["N_interactions"], r["N_cached"]] for r in rows if sel(r)])
+        y = np.array([r["ms_mean"] / 1e3 for r in rows if sel(r)])
+        return X, y
+
+    out = {}
+    for name, cats in (("appc", (1, 2, 3, 4, 5)), ("serving", (1, 2, 3, 4, 5, 6))):
+        Xtr, ytr = xy(lambda r: r["category"] in cats and r["split"] == "train")
+        Xte, yte = xy(lambda r: r["category"] in cats and r["split"] == "test")
+        lin = fit_ols(Xtr, ytr)
+        roof = fit_roofline(Xtr, ytr)
+        rec = {"linear": {"model": asdict(lin), "test": metrics(yte, lin.predict(Xte))},
+               "roofline": {"model": asdict(roof), "test": metrics(yte, roof.predict(Xte), 4)}}
+        if replay:
+            Xr = np.array([[r["N_linear"], r["N_interactions"], r["N_cached"]] for r in replay["rows"]])
+            yr = np.array([r["ms_mean"] / 1e3 for r in replay["rows"]])
+            rec["linear"]["replay"] = metrics(yr, lin.predict(Xr))
+            rec["roofline"]["replay"] = metrics(yr, roof.predict(Xr), 4)
+        out[name] = rec
+    return out
+
+
+def main(argv=None):
+    import argparse
+    ap = argparse.ArgumentParser(description="compare the linear and roofline-shaped estimators on a sweep")
+    ap.add_argument("sweep", help="latency-sweep record (latency_sweep --design serving)")
+    ap.add_argument("--replay", default="", help="replay record (latency_sweep --replay)")
+    ap.add_argument("--out", default="")
+    args = ap.parse_args(argv)
+    rec = compare_on_sweep(json.load(open(args.sweep)), json.load(open(args.replay)) if args.replay else None)
+    for name, r in rec.items():
+        for kind in ("linear", "roofline"):
+            t = r[kind]
+            extra = f", replay MAPE {t['replay']['mape_pct']:.1f} %" if "replay" in t else ""
+            print(f"{name:8s} {kind:9s}: test R2 {t['test']['r2']:.4f}, MAPE {t['test']['mape_pct']:.1f} %, "
+                  f"max err {1e3 * t['test']['max_err']:.2f} ms{extra}")
+    if args.out:
+        with open(args.out, "w") as f:
+            json.dump(rec, f, indent=1)
+
+
+if __name__ == "__main__":
+    main()

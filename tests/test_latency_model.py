@@ -2,6 +2,7 @@
 import os
 
 import numpy as np
+import pytest
 
 from paper_2601_11652_amd.latency_model import (LatencyModel, fit_ols, fit_report, kfold_r2, metrics,
                                                 step_features)
@@ -122,3 +123,22 @@ def test_serving_range_extension():
                 assert 128 <= ctx <= 3072 and 1 <= g <= 5 and pre == 0
     assert n_cold > 0
     assert max(sum(c.l_new) for c in six) <= ls.REPLAY_MAX_ROWS
+
+
+def test_roofline_variant_recovers_a_planted_knot():
+    """max(t_w, a N_linear) + b_c N_int + b_r N_cached + c: planted coefficients and knot
+    come back; with the knot below every N_linear it is the linear model, and its OLS."""
+    from paper_2601_11652_amd.latency_model import RooflineModel, fit_roofline
+    rng = np.random.default_rng(7)
+    n = 300
+    X = np.stack([rng.uniform(5, 3000, n), rng.uniform(1e3, 5e6, n), rng.uniform(0, 1e6, n)], 1)
+    true = RooflineModel(a=2.5e-5, knot=300.0, b_compute=1e-9, b_read=2e-8, c=1e-3)
+    y = true.predict(X) + rng.normal(0, 2e-5, n)
+    m = fit_roofline(X, y)
+    assert abs(m.knot - 300.0) / 300.0 < 0.05
+    np.testing.assert_allclose([m.a, m.b_compute, m.b_read, m.c], [2.5e-5, 1e-9, 2e-8, 1e-3], rtol=0.05, atol=3e-6)
+    # the time below the knot is flat: a * knot
+    assert m.predict([[10.0, 0, 0]])[0] == pytest.approx(m.a * m.knot + m.c, rel=1e-12)
+    lin = fit_roofline(X, X[:, :3] @ np.array([3e-5, 1e-9, 1e-8]) + 2e-3, knots=[0.0])
+    np.testing.assert_allclose([lin.a, lin.b_compute, lin.b_read, lin.c], [3e-5, 1e-9, 1e-8, 2e-3], rtol=1e-6)
+    assert fit_ols(X, y).coef.shape == (4,)
