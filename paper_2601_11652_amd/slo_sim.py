@@ -120,7 +120,8 @@ def simulate(n_devices: int, policy: int, model, model_err: float, *, sim_s: flo
              seed: int = 1, guard: float = 0.002, mem_budget: float = MAX_BATCH_ROWS, true_model=None,
              active=None, window: float = 0.0, keep_batches: int = 0):
     """One run.  `model` is what the scheduler estimates with; a batch really takes
-    `true_model` (default: `model`) times exp(N(0, model_err)).  `active(t)`, if given, is
+    `true_model` (default: `model`; a coefficient tuple of the same form, or any callable
+    (ctx_len array, l_new array) -> seconds) times exp(N(0, model_err)).  `active(t)`, if given, is
     the number of devices allowed to start a response at time t (devices 0 .. active-1).
     With `window` > 0 the result holds per-window compliance; `keep_batches` > 0 keeps an
     evenly spaced sample of that many batch compositions dispatched after the warm-up."""
@@ -190,7 +191,8 @@ def simulate(n_devices: int, policy: int, model, model_err: float, *, sim_s: flo
         if devs.shape[0] == 0:
             gpu_idle = True
             return
-        dur = batch_time(true_model, b["ctx_len"], b["l_new"])
+        dur = (true_model(b["ctx_len"], b["l_new"]) if callable(true_model)
+               else batch_time(true_model, b["ctx_len"], b["l_new"]))
         if model_err > 0:
             dur *= float(np.exp(rng.normal(0.0, model_err)))
         gpu_idle = False
@@ -304,6 +306,34 @@ def replay_batches(rec: dict) -> list:
     return r["batch_sample"]
 
 
+def roofline_time(rec: dict):
+    """The roofline-shaped estimator of a latency-model comparison record (serving fit) as a
+    batch-time function: max(a * knot, a * N_linear) + b_c N_int + b_r N_cached + c."""
+    m = rec["serving"]["roofline"]["model"]
+
+    def t(ctx, new):
+        ctx = np.asarray(ctx, np.float64)
+        new = np.asarray(new, np.float64)
+        return float(m["a"] * max(new.sum(), m["knot"]) + m["b_compute"] * ((ctx + new) * new).sum()
+                     + m["b_read"] * ctx.sum() + m["c"])
+    return t
+
+
+def robustness(model, truth, err, ns=(800, 1200, 1600), guards=(0.0, 0.002, 0.010, 0.030), sim_s=60.0):
+    """The scheduler estimating with `model` while batches take `truth` (times a lognormal
+    error `err`): violation and late shares per guard time (Sec. 4.4's guard against estimator
+    error), for the SLO policy with lost deadlines out of the critical queue."""
+    out = []
+    for N in ns:
+        for g in guards:
+            r = simulate(N, WISP_SCHED_SLO_LIVE, model, err, sim_s=sim_s, guard=g, true_model=truth)
+            out.append({"N": N, "guard_s": g, **{f"class_{int(c)}": {k: r[f"class_{int(c)}"][k] for k in
+                                                                   ("violation_share", "late_share")}
+                                                 for c in CLASSES},
+                        "goodput_tok_s": r["goodput_tok_s"], "mean_batch": r["mean_batch"]})
+    return out
+
+
 def capacity(rows, eps: float = 0.05) -> dict:
     """Per class, the largest swept N whose violation share is <= eps, with every smaller
     swept N within it too (Sec. 5's capacity)."""
@@ -400,6 +430,18 @@ def report(rec: dict, replay: dict | None = None) -> str:
             v = [w[f"class_{int(c)}"]["resp_met"] for w in r["windows"] if w[f"class_{int(c)}"]["resp_met"] is not None]
             cells.append(f"{100 * min(v):.0f} / {100 * float(np.mean(v)):.0f} %" if v else "-")
         L.append(f"| {name} | " + " | ".join(cells) + " |")
+    if rec.get("robustness"):
+        L.append("")
+        L.append("Estimator error (Sec. 4.4's guard time): the SLO policy with lost deadlines out of the critical "
+                 "queue estimates with the linear fit while batches take the roofline-shaped fit's time (a "
+                 "different, better model of this GPU), times the same lognormal error. Response violation % : "
+                 "late verification % per class:\n")
+        L.append("| N | guard (ms) | 2 tok/s | 4 tok/s | 6 tok/s | 8 tok/s | goodput | mean batch |")
+        L.append("|---|---|---|---|---|---|---|---|")
+        for x in rec["robustness"]:
+            L.append(f"| {x['N']} | {1e3 * x['guard_s']:.0f} | " + " | ".join(
+                f"{100 * x[f'class_{int(c)}']['violation_share']:.1f} : {100 * x[f'class_{int(c)}']['late_share']:.1f}"
+                for c in CLASSES) + f" | {x['goodput_tok_s']:.0f} | {x['mean_batch']:.0f} |")
     return "\n".join(L) + "\n"
 
 
@@ -412,6 +454,9 @@ def main(argv=None):
     ap.add_argument("--eps", type=float, default=0.05)
     ap.add_argument("--burst-period", type=float, default=120.0)
     ap.add_argument("--replay-n", type=int, default=120, help="batches kept for a GPU replay of the time model")
+    ap.add_argument("--roofline-json", default=os.path.join(root, "profiles", "latency_model_8b_roofline.json"),
+                    help="estimator comparison record whose roofline fit plays the true batch time in the "
+                         "robustness study ('' to skip)")
     ap.add_argument("--out", default="profiles/slo_sim_8b.json")
     ap.add_argument("--report", default="", help="only write the markdown summary of this record")
     ap.add_argument("--replay-record", default="", help="a GPU replay record to include in the summary")
@@ -459,6 +504,13 @@ def main(argv=None):
         print(f"{name} bursty (peak {peak} devices): worst-window response compliance {worst}", flush=True)
     # the GPU replay of the time model takes the batches the SLO scheduler dispatches at
     # FCFS's class-4 capacity (regenerated from these parameters by replay_batches)
+    if args.roofline_json:
+        rt = roofline_time(json.load(open(args.roofline_json)))
+        rec["robustness"] = robustness(model, rt, err)
+        for row in rec["robustness"]:
+            print(f"robustness N={row['N']:5d} guard {1e3 * row['guard_s']:4.0f} ms: " + " ".join(
+                f"c{int(c)} {100 * row[f'class_{int(c)}']['violation_share']:5.1f}%/"
+                f"{100 * row[f'class_{int(c)}']['late_share']:4.1f}%" for c in CLASSES), flush=True)
     rec["replay_N"] = max(rec["capacity"]["fcfs"]["class_8"], ns[0])
     rec["replay_n"] = args.replay_n
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
