@@ -46,6 +46,8 @@ typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
 #define WISP_PAGE 16        /* tokens per KV page                                            */
 #define WISP_GAMMA_MAX 16   /* most draft tokens per request                                 */
 #define WISP_PREFILL_MAX 32768 /* most uncached prompt tokens per request and call (prefill_len) */
+#define WISP_ROWS_MAX 262144  /* most rows per call: sum of prefill_len + gamma + 1 (wisp_accept:
+                                 sum of gamma + 1); WISP_E_UNSUPPORTED beyond            */
 
 /*
  * Decoder-only transformer (RMSNorm, rotary embedding with rotate-half pairing,
@@ -166,6 +168,9 @@ wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t c
  * a rejection (or z = logits/T when the residual is empty), z after full acceptance.
  * Device-side input faults (token id outside [0, vocab), block id outside
  * [0, n_blocks)) are recorded in the workspace and reported by wisp_check().
+ * Batches of more than WISP_ROWS_MAX rows, or whose contexts would need more than 2^22
+ * split-KV work items (about 2^22 x 1024 tokens summed over requests, kv heads and
+ * 48-row groups), return WISP_E_UNSUPPORTED; the workspace sizes are then 0.
  */
 wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
                         const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,

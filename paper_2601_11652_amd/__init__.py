@@ -32,6 +32,8 @@ WISP_F32 = 0
 WISP_BF16 = 1
 PAGE = 16
 GAMMA_MAX = 16
+PREFILL_MAX = 32768
+ROWS_MAX = 262144
 TAG_ACCEPT = 1
 TAG_RACE = 2
 

@@ -83,6 +83,7 @@ struct AttnGroup {  // the chunks of one (request, kv head, row group), combined
   int32_t req, kvh, rbg, first_item, n_items, pad0, pad1, pad2;
 };
 constexpr int kAttnRowsPerItem = 48;   // query rows one wave carries (3 blocks of 16)
+constexpr int kAttnMaxItems = 1 << 22;  // split-KV work items of one call (int indices, workspace)
 constexpr int kAttnMaxChunkPages = 64; // pages of one item (one block id per lane)
 
 // split-KV partials of every item, then their fixed-order combine into `out`

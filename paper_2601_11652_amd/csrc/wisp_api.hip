@@ -86,12 +86,14 @@ wisp_status check_model(const wisp_model *m, bool need_weights) {
   return WISP_OK;
 }
 
-wisp_status check_desc(const wisp_batch_desc *d, bool need_pages) {
+// forward: the call runs the model, so prompt rows count towards the batch's rows
+wisp_status check_desc(const wisp_batch_desc *d, bool need_pages, bool forward) {
   if (!d) return fail(WISP_E_INVALID, "batch descriptor is NULL");
   if (d->B < 0) return fail(WISP_E_INVALID, "B < 0");
   if (d->B == 0) return WISP_OK;
   if (!d->ctx_len || !d->gamma) return fail(WISP_E_INVALID, "ctx_len / gamma is NULL");
   if (!(d->temperature >= 0.f) || std::isinf(d->temperature)) return fail(WISP_E_INVALID, "temperature must be finite and >= 0");
+  int64_t rows = 0;
   for (int i = 0; i < d->B; ++i) {
     if (d->gamma[i] < 0 || d->gamma[i] > WISP_GAMMA_MAX)
       return fail(WISP_E_INVALID, "gamma[%d] = %d outside 0..%d", i, d->gamma[i], WISP_GAMMA_MAX);
@@ -104,6 +106,9 @@ wisp_status check_desc(const wisp_batch_desc *d, bool need_pages) {
     if (need_pages && (int64_t)d->pt_stride * WISP_PAGE < need)
       return fail(WISP_E_CAPACITY, "request %d needs %lld tokens but the page table holds %d", i,
                   (long long)need, d->pt_stride * WISP_PAGE);
+    rows += (forward ? pre : 0) + d->gamma[i] + 1;
+    if (rows > WISP_ROWS_MAX)
+      return fail(WISP_E_UNSUPPORTED, "the batch has more than %d rows (prompt, root and draft rows)", WISP_ROWS_MAX);
   }
   if (need_pages && !d->kv_page_table) return fail(WISP_E_INVALID, "kv_page_table is NULL");
   return WISP_OK;
@@ -124,7 +129,7 @@ int device_cus() {
   return n;
 }
 
-void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward, int vocab = 0) {
+wisp_status make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forward, int vocab = 0) {
   p.B = d->B;
   p.V = forward ? m->vocab : vocab;
   // rows of request i: prefill_len prompt rows (forward only), root, gamma drafts; the
@@ -192,6 +197,10 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
       const int L_max = kAttnMaxChunkPages / 2;
       int64_t rounds = 1;
       const int64_t fewest = count_items(L_max);
+      // the work list holds at most fewest + slots items (below); its indices are int
+      if (fewest > kAttnMaxItems - slots)
+        return fail(WISP_E_UNSUPPORTED, "the batch's contexts need %lld attention work items (at most %d)",
+                    (long long)fewest, kAttnMaxItems - (int)slots);
       while (rounds * slots < fewest) ++rounds;
       int L = 2;
       while (L < L_max && count_items(L) > rounds * slots) ++L;
@@ -292,6 +301,7 @@ void make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bool forw
     carve(p, w, p.w_attn_ml, p.items.size() * 64 * 2 * 4);
   }
   p.total = w;
+  return WISP_OK;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -565,23 +575,23 @@ extern "C" {
 const char *wisp_last_error(void) { return g_last_error.c_str(); }
 
 size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc) {
-  if (check_model(model, false) != WISP_OK || check_desc(desc, false) != WISP_OK) return 0;
+  if (check_model(model, false) != WISP_OK || check_desc(desc, false, true) != WISP_OK) return 0;
   Plan p;
-  make_plan(p, model, desc, true);
+  if (make_plan(p, model, desc, true) != WISP_OK) return 0;
   return p.total;
 }
 
 size_t wisp_logits_workspace_size(const wisp_model *model, const wisp_batch_desc *desc) {
-  if (check_model(model, false) != WISP_OK || check_desc(desc, false) != WISP_OK) return 0;
+  if (check_model(model, false) != WISP_OK || check_desc(desc, false, true) != WISP_OK) return 0;
   Plan p;
-  make_plan(p, model, desc, true);
+  if (make_plan(p, model, desc, true) != WISP_OK) return 0;
   return align256((size_t)p.Mv * (size_t)p.V * sizeof(float));
 }
 
 size_t wisp_accept_workspace_size(const wisp_batch_desc *desc, int32_t vocab) {
-  if (check_desc(desc, false) != WISP_OK || vocab <= 0) return 0;
+  if (check_desc(desc, false, false) != WISP_OK || vocab <= 0) return 0;
   Plan p;
-  make_plan(p, nullptr, desc, false, vocab);
+  if (make_plan(p, nullptr, desc, false, vocab) != WISP_OK) return 0;
   return p.total;
 }
 
@@ -608,7 +618,7 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
                         void *workspace, size_t workspace_bytes, void *stream) {
   wisp_status st;
   if ((st = check_model(model, true)) != WISP_OK) return st;
-  if ((st = check_desc(desc, true)) != WISP_OK) return st;
+  if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
   if (desc->B == 0) return WISP_OK;
   if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
   if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
@@ -616,7 +626,7 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
   if (!tokens || !accept_len || !out_tokens || !workspace)
     return fail(WISP_E_INVALID, "NULL tokens / outputs / workspace");
   Plan p;
-  make_plan(p, model, desc, true);
+  if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
   if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
   if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
   // without a caller buffer the logits live in the workspace, after everything else
@@ -657,13 +667,13 @@ wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float 
                         int32_t *accept_len, int32_t *out_tokens, void *workspace,
                         size_t workspace_bytes, void *stream) {
   wisp_status st;
-  if ((st = check_desc(desc, false)) != WISP_OK) return st;
+  if ((st = check_desc(desc, false, false)) != WISP_OK) return st;
   if (desc->B == 0) return WISP_OK;
   if (vocab <= 0) return fail(WISP_E_INVALID, "vocab must be positive");
   if (!logits || !tokens || !accept_len || !out_tokens || !workspace)
     return fail(WISP_E_INVALID, "NULL logits / tokens / outputs / workspace");
   Plan p;
-  make_plan(p, nullptr, desc, false, vocab);
+  if ((st = make_plan(p, nullptr, desc, false, vocab)) != WISP_OK) return st;
   if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
   if (workspace_bytes < p.total)
     return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
@@ -682,13 +692,13 @@ wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wis
                            void *stream) {
   wisp_status st;
   if ((st = check_model(model, false)) != WISP_OK) return st;
-  if ((st = check_desc(desc, true)) != WISP_OK) return st;
+  if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
   if (desc->B == 0) return WISP_OK;
   if (!kv || !kv->k_pool || !kv->v_pool || kv->n_blocks <= 0) return fail(WISP_E_INVALID, "KV pools");
   if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
   if (!q || !out || !workspace) return fail(WISP_E_INVALID, "NULL q / out / workspace");
   Plan p;
-  make_plan(p, model, desc, true);
+  if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
   if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
   if (workspace_bytes < p.total)
     return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);

@@ -99,6 +99,41 @@ def test_prefill_validation_and_sizes(W):
     assert d.M == 6 and d.rows == 48
 
 
+def test_batch_size_limits(W):
+    """Totals that the plan keeps in int: at most ROWS_MAX rows per call (prompt rows count
+    only where the model runs) and at most 2^22 split-KV work items; beyond either the call
+    returns WISP_E_UNSUPPORTED and the workspace sizes are 0."""
+    m = _model(W)
+    n = W.ROWS_MAX // (W.PREFILL_MAX + 1)                 # requests of a full prompt that fit
+    fits = _desc(W, [0] * n, [0] * n, stride=4096, prefill=[W.PREFILL_MAX] * n)
+    over = _desc(W, [0] * (n + 1), [0] * (n + 1), stride=4096, prefill=[W.PREFILL_MAX] * (n + 1))
+    assert n * (W.PREFILL_MAX + 1) <= W.ROWS_MAX < (n + 1) * (W.PREFILL_MAX + 1)
+    assert W.wisp_workspace_size(m, fits) > 0
+    assert W.wisp_workspace_size(m, over) == 0
+    assert W.wisp_logits_workspace_size(m, over) == 0
+    assert _verify(W, m, over) == W.WISP_E_UNSUPPORTED
+    assert "rows" in W.wisp_last_error()
+    # the acceptance stage ignores prompt rows
+    assert W.wisp_accept_workspace_size(over, 1024) > 0
+    # exactly ROWS_MAX rows pass, one more does not (drafts only)
+    B = W.ROWS_MAX // (W.GAMMA_MAX + 1)
+    tail = W.ROWS_MAX - B * (W.GAMMA_MAX + 1)
+    gam = [W.GAMMA_MAX] * B + ([tail - 1] if tail else [])
+    assert sum(g + 1 for g in gam) == W.ROWS_MAX
+    assert W.wisp_accept_workspace_size(_desc(W, [0] * len(gam), gam), 1024) > 0
+    assert W.wisp_accept_workspace_size(_desc(W, [0] * (len(gam) + 1), gam + [0]), 1024) == 0
+    # contexts whose split-KV work list would pass 2^22 items (bf16 path: 1024 tokens
+    # per item at most, one item list per kv head and 48-row group)
+    mb = _model(W, dtype=W.WISP_BF16)
+    ctx = 1 << 29                                         # 2^19 items per kv head
+    few = _desc(W, [ctx] * 1, [0], stride=(ctx >> 4) + 1)
+    many = _desc(W, [ctx] * 2, [0, 0], stride=(ctx >> 4) + 1)   # 2 x 4 heads x 2^19 = 2^22
+    assert W.wisp_workspace_size(mb, few) > 0
+    assert W.wisp_workspace_size(mb, many) == 0
+    assert _verify(W, mb, many) == W.WISP_E_UNSUPPORTED
+    assert "work items" in W.wisp_last_error()
+
+
 def test_workspace_size_and_pack_validation(W):
     m = _model(W)
     assert W.wisp_workspace_size(m, _desc(W, [10], [2])) > 0
