@@ -38,7 +38,8 @@ typedef enum {
   WISP_E_WORKSPACE = -3,    /* workspace smaller than wisp_workspace_size()                  */
   WISP_E_UNSUPPORTED = -4,  /* shape outside what the kernels implement                      */
   WISP_E_HIP = -5,          /* HIP runtime error                                             */
-  WISP_E_DEVICE_INPUT = -6  /* a device-side input check failed (token id, block id)         */
+  WISP_E_DEVICE_INPUT = -6, /* a device-side input check failed (token id, block id)         */
+  WISP_E_HOST_MEMORY = -7   /* host memory exhausted while planning or bookkeeping           */
 } wisp_status;
 
 typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
@@ -316,7 +317,8 @@ wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *requests, in
  *   wisp_kvm_release  forgets the sessions and frees their pages (unknown ids ignored).
  * reserve and commit mark their sessions as used (one clock tick per call).  Errors:
  * WISP_E_INVALID for NULL pointers, n < 0, a session twice in one call, n_tokens below
- * the cached tokens, or a commit outside the reserved pages.
+ * the cached tokens, or a commit outside the reserved pages; WISP_E_HOST_MEMORY when the
+ * manager's host bookkeeping cannot grow (the manager is then only fit for destroy).
  */
 typedef struct wisp_kv_manager wisp_kv_manager;
 

@@ -28,6 +28,7 @@ WISP_E_WORKSPACE = -3
 WISP_E_UNSUPPORTED = -4
 WISP_E_HIP = -5
 WISP_E_DEVICE_INPUT = -6
+WISP_E_HOST_MEMORY = -7
 WISP_F32 = 0
 WISP_BF16 = 1
 PAGE = 16

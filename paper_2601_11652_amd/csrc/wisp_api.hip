@@ -13,22 +13,22 @@
 
 #include "../../include/wisp.h"
 #include "common.h"
+#include "host_guard.h"
 #include "kernels.h"
 
 using namespace wisp;
 
 namespace {
 
-thread_local std::string g_last_error;
+// the calling thread's last error message (a fixed buffer: reporting never allocates)
+thread_local char g_last_error[512] = "";
 
 wisp_status fail(wisp_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 wisp_status fail(wisp_status st, const char *fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return st;
 }
 
@@ -563,8 +563,12 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
 }  // namespace
 
 namespace wisp {
-// lets the host-only sources (the scheduler) report through wisp_last_error
+// lets the host-only sources (the scheduler, the KV manager) report through wisp_last_error
 wisp_status report_error(wisp_status st, const char *msg) { return fail(st, "%s", msg); }
+wisp_status report_exception(const char *who, bool out_of_memory) {
+  return out_of_memory ? fail(WISP_E_HOST_MEMORY, "%s: host memory exhausted", who)
+                       : fail(WISP_E_INVALID, "%s: unexpected host-side exception", who);
+}
 }  // namespace wisp
 
 // ------------------------------------------------------------------------------------------
@@ -572,204 +576,228 @@ wisp_status report_error(wisp_status st, const char *msg) { return fail(st, "%s"
 // ------------------------------------------------------------------------------------------
 extern "C" {
 
-const char *wisp_last_error(void) { return g_last_error.c_str(); }
+const char *wisp_last_error(void) { return g_last_error; }
 
 size_t wisp_workspace_size(const wisp_model *model, const wisp_batch_desc *desc) {
-  if (check_model(model, false) != WISP_OK || check_desc(desc, false, true) != WISP_OK) return 0;
-  Plan p;
-  if (make_plan(p, model, desc, true) != WISP_OK) return 0;
-  return p.total;
+  return guarded_size([&]() -> size_t {
+    if (check_model(model, false) != WISP_OK || check_desc(desc, false, true) != WISP_OK) return 0;
+    Plan p;
+    if (make_plan(p, model, desc, true) != WISP_OK) return 0;
+    return p.total;
+  });
 }
 
 size_t wisp_logits_workspace_size(const wisp_model *model, const wisp_batch_desc *desc) {
-  if (check_model(model, false) != WISP_OK || check_desc(desc, false, true) != WISP_OK) return 0;
-  Plan p;
-  if (make_plan(p, model, desc, true) != WISP_OK) return 0;
-  return align256((size_t)p.Mv * (size_t)p.V * sizeof(float));
+  return guarded_size([&]() -> size_t {
+    if (check_model(model, false) != WISP_OK || check_desc(desc, false, true) != WISP_OK) return 0;
+    Plan p;
+    if (make_plan(p, model, desc, true) != WISP_OK) return 0;
+    return align256((size_t)p.Mv * (size_t)p.V * sizeof(float));
+  });
 }
 
 size_t wisp_accept_workspace_size(const wisp_batch_desc *desc, int32_t vocab) {
-  if (check_desc(desc, false, false) != WISP_OK || vocab <= 0) return 0;
-  Plan p;
-  if (make_plan(p, nullptr, desc, false, vocab) != WISP_OK) return 0;
-  return p.total;
+  return guarded_size([&]() -> size_t {
+    if (check_desc(desc, false, false) != WISP_OK || vocab <= 0) return 0;
+    Plan p;
+    if (make_plan(p, nullptr, desc, false, vocab) != WISP_OK) return 0;
+    return p.total;
+  });
 }
 
 wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t cols, int32_t dtype,
                              void *stream) {
-  if (!dst || !src) return fail(WISP_E_INVALID, "NULL pointer");
-  if (rows <= 0 || cols <= 0) return fail(WISP_E_INVALID, "rows, cols must be positive");
-  hipStream_t s = (hipStream_t)stream;
-  if (dtype == WISP_BF16) {
-    if (rows % 32 || cols % 16) return fail(WISP_E_UNSUPPORTED, "bf16 packing needs rows %% 32 == 0 and cols %% 16 == 0");
-    pack_linear_bf16((uint16_t *)dst, (const uint16_t *)src, rows, cols, s);
-  } else if (dtype == WISP_F32) {
-    if (hipMemcpyAsync(dst, src, (size_t)rows * cols * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
-      return fail(WISP_E_HIP, "copy failed");
-  } else {
-    return fail(WISP_E_UNSUPPORTED, "dtype %d", dtype);
-  }
-  return hip_check("pack");
+  return guarded("wisp_pack_linear", [&]() -> wisp_status {
+    if (!dst || !src) return fail(WISP_E_INVALID, "NULL pointer");
+    if (rows <= 0 || cols <= 0) return fail(WISP_E_INVALID, "rows, cols must be positive");
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == WISP_BF16) {
+      if (rows % 32 || cols % 16) return fail(WISP_E_UNSUPPORTED, "bf16 packing needs rows %% 32 == 0 and cols %% 16 == 0");
+      pack_linear_bf16((uint16_t *)dst, (const uint16_t *)src, rows, cols, s);
+    } else if (dtype == WISP_F32) {
+      if (hipMemcpyAsync(dst, src, (size_t)rows * cols * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return fail(WISP_E_HIP, "copy failed");
+    } else {
+      return fail(WISP_E_UNSUPPORTED, "dtype %d", dtype);
+    }
+    return hip_check("pack");
+  });
 }
 
 wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
                         const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
                         int32_t *accept_len, int32_t *out_tokens, float *target_logits,
                         void *workspace, size_t workspace_bytes, void *stream) {
-  wisp_status st;
-  if ((st = check_model(model, true)) != WISP_OK) return st;
-  if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
-  if (desc->B == 0) return WISP_OK;
-  if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
-  if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
-  if (kv->n_blocks <= 0) return fail(WISP_E_INVALID, "n_blocks must be positive");
-  if (!tokens || !accept_len || !out_tokens || !workspace)
-    return fail(WISP_E_INVALID, "NULL tokens / outputs / workspace");
-  Plan p;
-  if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
-  if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
-  if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
-  // without a caller buffer the logits live in the workspace, after everything else
-  const size_t need = p.total + (target_logits ? 0 : align256((size_t)p.Mv * (size_t)p.V * sizeof(float)));
-  if (workspace_bytes < need)
-    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
-  hipStream_t s = (hipStream_t)stream;
-  char *ws = (char *)workspace;
-  if (!target_logits) target_logits = reinterpret_cast<float *>(ws + p.total);
-  if ((st = upload(p, ws, s)) != WISP_OK) return st;
-  StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
-  clear_ints(sd.err, 1, s);
-  if (p.bf16)
-    st = run_forward<uint16_t>(p, model, kv, sd, ws, tokens, target_logits, s);
-  else
-    st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
-  if (st != WISP_OK) return st;
-  {
-    // the acceptance sees the verification rows only: row offsets over them, and (with
-    // prompt rows present) their tokens gathered into a compact array
-    StepDesc sv = sd;
-    sv.off = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_voff;
-    const int32_t *vtok = tokens;
-    if (p.prefill) {
-      int32_t *g = reinterpret_cast<int32_t *>(ws + p.w_vtok);
-      gather_ints(tokens, reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow, p.Mv, g, s);
-      vtok = g;
+  return guarded("wisp_verify", [&]() -> wisp_status {
+    wisp_status st;
+    if ((st = check_model(model, true)) != WISP_OK) return st;
+    if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
+    if (desc->B == 0) return WISP_OK;
+    if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
+    if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
+    if (kv->n_blocks <= 0) return fail(WISP_E_INVALID, "n_blocks must be positive");
+    if (!tokens || !accept_len || !out_tokens || !workspace)
+      return fail(WISP_E_INVALID, "NULL tokens / outputs / workspace");
+    Plan p;
+    if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
+    if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
+    if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
+    // without a caller buffer the logits live in the workspace, after everything else
+    const size_t need = p.total + (target_logits ? 0 : align256((size_t)p.Mv * (size_t)p.V * sizeof(float)));
+    if (workspace_bytes < need)
+      return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+    hipStream_t s = (hipStream_t)stream;
+    char *ws = (char *)workspace;
+    if (!target_logits) target_logits = reinterpret_cast<float *>(ws + p.total);
+    if ((st = upload(p, ws, s)) != WISP_OK) return st;
+    StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
+    clear_ints(sd.err, 1, s);
+    if (p.bf16)
+      st = run_forward<uint16_t>(p, model, kv, sd, ws, tokens, target_logits, s);
+    else
+      st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
+    if (st != WISP_OK) return st;
+    {
+      // the acceptance sees the verification rows only: row offsets over them, and (with
+      // prompt rows present) their tokens gathered into a compact array
+      StepDesc sv = sd;
+      sv.off = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_voff;
+      const int32_t *vtok = tokens;
+      if (p.prefill) {
+        int32_t *g = reinterpret_cast<int32_t *>(ws + p.w_vtok);
+        gather_ints(tokens, reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow, p.Mv, g, s);
+        vtok = g;
+      }
+      ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
+      sampler(sv, p.B, p.Mv, p.V, target_logits, vtok, draft_probs, desc->temperature, rng_seed,
+              sampler_scratch(p, ws), accept_len, out_tokens, s);
     }
-    ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
-    sampler(sv, p.B, p.Mv, p.V, target_logits, vtok, draft_probs, desc->temperature, rng_seed,
-            sampler_scratch(p, ws), accept_len, out_tokens, s);
-  }
-  return hip_check("sampler launch");
+    return hip_check("sampler launch");
+  });
 }
 
 wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float *logits,
                         const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
                         int32_t *accept_len, int32_t *out_tokens, void *workspace,
                         size_t workspace_bytes, void *stream) {
-  wisp_status st;
-  if ((st = check_desc(desc, false, false)) != WISP_OK) return st;
-  if (desc->B == 0) return WISP_OK;
-  if (vocab <= 0) return fail(WISP_E_INVALID, "vocab must be positive");
-  if (!logits || !tokens || !accept_len || !out_tokens || !workspace)
-    return fail(WISP_E_INVALID, "NULL logits / tokens / outputs / workspace");
-  Plan p;
-  if ((st = make_plan(p, nullptr, desc, false, vocab)) != WISP_OK) return st;
-  if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
-  if (workspace_bytes < p.total)
-    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
-  hipStream_t s = (hipStream_t)stream;
-  char *ws = (char *)workspace;
-  if ((st = upload(p, ws, s)) != WISP_OK) return st;
-  StepDesc sd = step_desc(p, ws, desc, 0);
-  clear_ints(sd.err, 1, s);
-  sampler(sd, p.B, p.M, vocab, logits, tokens, draft_probs, desc->temperature, rng_seed,
-          sampler_scratch(p, ws), accept_len, out_tokens, s);
-  return hip_check("sampler launch");
+  return guarded("wisp_accept", [&]() -> wisp_status {
+    wisp_status st;
+    if ((st = check_desc(desc, false, false)) != WISP_OK) return st;
+    if (desc->B == 0) return WISP_OK;
+    if (vocab <= 0) return fail(WISP_E_INVALID, "vocab must be positive");
+    if (!logits || !tokens || !accept_len || !out_tokens || !workspace)
+      return fail(WISP_E_INVALID, "NULL logits / tokens / outputs / workspace");
+    Plan p;
+    if ((st = make_plan(p, nullptr, desc, false, vocab)) != WISP_OK) return st;
+    if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
+    if (workspace_bytes < p.total)
+      return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
+    hipStream_t s = (hipStream_t)stream;
+    char *ws = (char *)workspace;
+    if ((st = upload(p, ws, s)) != WISP_OK) return st;
+    StepDesc sd = step_desc(p, ws, desc, 0);
+    clear_ints(sd.err, 1, s);
+    sampler(sd, p.B, p.M, vocab, logits, tokens, draft_probs, desc->temperature, rng_seed,
+            sampler_scratch(p, ws), accept_len, out_tokens, s);
+    return hip_check("sampler launch");
+  });
 }
 
 wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
                            const void *q, void *out, void *workspace, size_t workspace_bytes,
                            void *stream) {
-  wisp_status st;
-  if ((st = check_model(model, false)) != WISP_OK) return st;
-  if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
-  if (desc->B == 0) return WISP_OK;
-  if (!kv || !kv->k_pool || !kv->v_pool || kv->n_blocks <= 0) return fail(WISP_E_INVALID, "KV pools");
-  if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
-  if (!q || !out || !workspace) return fail(WISP_E_INVALID, "NULL q / out / workspace");
-  Plan p;
-  if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
-  if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
-  if (workspace_bytes < p.total)
-    return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
-  hipStream_t s = (hipStream_t)stream;
-  char *ws = (char *)workspace;
-  if ((st = upload(p, ws, s)) != WISP_OK) return st;
-  StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
-  clear_ints(sd.err, 1, s);
-  if (p.bf16) {
-    const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
-    const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
-    float *po = reinterpret_cast<float *>(ws + p.w_attn_o);
-    float *pml = reinterpret_cast<float *>(ws + p.w_attn_ml);
-    attention_bf16_main(sd, items, (int)p.items.size(), (const uint16_t *)q, (const uint16_t *)kv->k_pool,
-                        (const uint16_t *)kv->v_pool, po, pml, p.nq, p.nkv, p.hd, s);
-    attention_bf16_combine(sd, groups, (int)p.groups.size(), po, pml, (uint16_t *)out, false, p.qdim, p.nq,
-                           p.nkv, p.hd, s);
-  } else {
-    attention_f32(sd, p.B, (const float *)q, (const float *)kv->k_pool, (const float *)kv->v_pool,
-                  (float *)out, p.nq, p.nkv, p.hd, p.max_tokens, s);
-  }
-  return hip_check("attention launch");
+  return guarded("wisp_attention", [&]() -> wisp_status {
+    wisp_status st;
+    if ((st = check_model(model, false)) != WISP_OK) return st;
+    if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
+    if (desc->B == 0) return WISP_OK;
+    if (!kv || !kv->k_pool || !kv->v_pool || kv->n_blocks <= 0) return fail(WISP_E_INVALID, "KV pools");
+    if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
+    if (!q || !out || !workspace) return fail(WISP_E_INVALID, "NULL q / out / workspace");
+    Plan p;
+    if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
+    if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
+    if (workspace_bytes < p.total)
+      return fail(WISP_E_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.total);
+    hipStream_t s = (hipStream_t)stream;
+    char *ws = (char *)workspace;
+    if ((st = upload(p, ws, s)) != WISP_OK) return st;
+    StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
+    clear_ints(sd.err, 1, s);
+    if (p.bf16) {
+      const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
+      const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
+      float *po = reinterpret_cast<float *>(ws + p.w_attn_o);
+      float *pml = reinterpret_cast<float *>(ws + p.w_attn_ml);
+      attention_bf16_main(sd, items, (int)p.items.size(), (const uint16_t *)q, (const uint16_t *)kv->k_pool,
+                          (const uint16_t *)kv->v_pool, po, pml, p.nq, p.nkv, p.hd, s);
+      attention_bf16_combine(sd, groups, (int)p.groups.size(), po, pml, (uint16_t *)out, false, p.qdim, p.nq,
+                             p.nkv, p.hd, s);
+    } else {
+      attention_f32(sd, p.B, (const float *)q, (const float *)kv->k_pool, (const float *)kv->v_pool,
+                    (float *)out, p.nq, p.nkv, p.hd, p.max_tokens, s);
+    }
+    return hip_check("attention launch");
+  });
 }
 
 wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint32_t row, uint32_t n,
                          float *out, void *stream) {
-  if (!out && n) return fail(WISP_E_INVALID, "out is NULL");
-  uniform_draws(rng_seed, req_id, tag, row, n, out, (hipStream_t)stream);
-  return hip_check("uniform launch");
+  return guarded("wisp_uniform", [&]() -> wisp_status {
+    if (!out && n) return fail(WISP_E_INVALID, "out is NULL");
+    uniform_draws(rng_seed, req_id, tag, row, n, out, (hipStream_t)stream);
+    return hip_check("uniform launch");
+  });
 }
 
 wisp_status wisp_profile_enable(int on) {
-  if (!on) prof_collect();
-  g_prof.on = on != 0;
-  return WISP_OK;
+  return guarded("wisp_profile_enable", [&]() -> wisp_status {
+    if (!on) prof_collect();
+    g_prof.on = on != 0;
+    return WISP_OK;
+  });
 }
 
 wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops) {
-  if (kind < 0 || kind >= WISP_PROF_KINDS) return fail(WISP_E_INVALID, "profile kind %d", kind);
-  prof_collect();
-  if (ms) *ms = g_prof.ms[kind];
-  if (launches) *launches = g_prof.launches[kind];
-  if (bytes) *bytes = g_prof.bytes[kind];
-  if (flops) *flops = g_prof.flops[kind];
-  return WISP_OK;
+  return guarded("wisp_profile_read", [&]() -> wisp_status {
+    if (kind < 0 || kind >= WISP_PROF_KINDS) return fail(WISP_E_INVALID, "profile kind %d", kind);
+    prof_collect();
+    if (ms) *ms = g_prof.ms[kind];
+    if (launches) *launches = g_prof.launches[kind];
+    if (bytes) *bytes = g_prof.bytes[kind];
+    if (flops) *flops = g_prof.flops[kind];
+    return WISP_OK;
+  });
 }
 
 wisp_status wisp_profile_reset(void) {
-  prof_collect();
-  for (int k = 0; k < WISP_PROF_KINDS; ++k) {
-    g_prof.ms[k] = g_prof.bytes[k] = g_prof.flops[k] = 0.0;
-    g_prof.launches[k] = 0;
-  }
-  return WISP_OK;
+  return guarded("wisp_profile_reset", [&]() -> wisp_status {
+    prof_collect();
+    for (int k = 0; k < WISP_PROF_KINDS; ++k) {
+      g_prof.ms[k] = g_prof.bytes[k] = g_prof.flops[k] = 0.0;
+      g_prof.launches[k] = 0;
+    }
+    return WISP_OK;
+  });
 }
 
 wisp_status wisp_check(void *workspace, void *stream) {
-  if (!workspace) return fail(WISP_E_INVALID, "workspace is NULL");
-  hipStream_t s = (hipStream_t)stream;
-  if (hipStreamSynchronize(s) != hipSuccess) return fail(WISP_E_HIP, "stream synchronize failed");
-  int err = 0;
-  if (hipMemcpy(&err, workspace, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
-    return fail(WISP_E_HIP, "error word read failed");
-  if (err) {
-    int zero = 0;
-    (void)hipMemcpy(workspace, &zero, sizeof(int), hipMemcpyHostToDevice);
-    return fail(WISP_E_DEVICE_INPUT, "device-side input check failed:%s%s",
-                (err & kErrToken) ? " token id out of range" : "",
-                (err & kErrBlock) ? " block id out of range" : "");
-  }
-  return WISP_OK;
+  return guarded("wisp_check", [&]() -> wisp_status {
+    if (!workspace) return fail(WISP_E_INVALID, "workspace is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    if (hipStreamSynchronize(s) != hipSuccess) return fail(WISP_E_HIP, "stream synchronize failed");
+    int err = 0;
+    if (hipMemcpy(&err, workspace, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+      return fail(WISP_E_HIP, "error word read failed");
+    if (err) {
+      int zero = 0;
+      (void)hipMemcpy(workspace, &zero, sizeof(int), hipMemcpyHostToDevice);
+      return fail(WISP_E_DEVICE_INPUT, "device-side input check failed:%s%s",
+                  (err & kErrToken) ? " token id out of range" : "",
+                  (err & kErrBlock) ? " block id out of range" : "");
+    }
+    return WISP_OK;
+  });
 }
 
 }  // extern "C"
