@@ -47,8 +47,9 @@ typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
 #define WISP_PAGE 16        /* tokens per KV page                                            */
 #define WISP_GAMMA_MAX 16   /* most draft tokens per request                                 */
 #define WISP_PREFILL_MAX 32768 /* most uncached prompt tokens per request and call (prefill_len) */
-#define WISP_ROWS_MAX 262144  /* most rows per call: sum of prefill_len + gamma + 1 (wisp_accept:
-                                 sum of gamma + 1); WISP_E_UNSUPPORTED beyond            */
+#define WISP_ROWS_MAX 262144  /* most rows per model call (wisp_verify, wisp_attention): sum of
+                                 prefill_len + gamma + 1; WISP_E_UNSUPPORTED beyond.  The
+                                 acceptance alone (wisp_accept) takes up to 2^29 rows.    */
 
 /*
  * Decoder-only transformer (RMSNorm, rotary embedding with rotate-half pairing,

@@ -183,6 +183,50 @@ def _ptr(t) -> int | None:
     return t.data_ptr()
 
 
+def _dev(t, what: str, numel: int = 0, dtype=None, elem: int | None = None, contiguous: bool = True) -> int:
+    """Device pointer of a torch tensor after the checks a C caller would owe the library:
+    on the GPU, of the element type the entry point reads, contiguous, and holding at least
+    `numel` elements.  A host tensor's pointer must never reach a kernel."""
+    import torch
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{what}: expected a device tensor, got {type(t).__name__}"
+                         + (f" on {t.device}" if isinstance(t, torch.Tensor) else ""))
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what}: dtype {t.dtype}, expected {dtype}")
+    if elem is not None and t.element_size() != elem:
+        raise ValueError(f"{what}: {t.element_size()}-byte elements, expected {elem}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{what}: must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{what}: {t.numel()} elements, needs at least {numel}")
+    return t.data_ptr()
+
+
+def _i32():
+    import torch
+    return torch.int32
+
+
+def _f32():
+    import torch
+    return torch.float32
+
+
+def _check_kv(model: "wisp_model", kv: "KVPool", layers: int):
+    es = 2 if model.dtype == WISP_BF16 else 4
+    per_layer = kv.c.n_blocks * model.n_kv_heads * PAGE * model.head_dim
+    for name, t in (("kv.k", kv.k), ("kv.v", kv.v)):
+        _dev(t, name, layers * per_layer, elem=es)
+
+
+def _check_desc(desc: "BatchDesc"):
+    if desc.B > 0:
+        pt = desc.page_table
+        _dev(pt, "desc.page_table", dtype=_i32())
+        if pt.dim() != 2 or pt.shape[0] < desc.B:
+            raise ValueError(f"desc.page_table: expected [>= {desc.B}][pt_stride], got {tuple(pt.shape)}")
+
+
 def _stream(stream) -> int | None:
     if stream is None:
         import torch
@@ -340,30 +384,51 @@ def wisp_accept_workspace_size(desc: BatchDesc, vocab: int) -> int:
 
 
 def wisp_pack_linear(dst, src, rows: int, cols: int, dtype: int, stream=None):
-    _ok(lib.wisp_pack_linear(_ptr(dst), _ptr(src), rows, cols, dtype, _stream(stream)))
+    es = 2 if dtype == WISP_BF16 else 4
+    n = max(rows, 0) * max(cols, 0)
+    _ok(lib.wisp_pack_linear(_dev(dst, "dst", n, elem=es), _dev(src, "src", n, elem=es), rows, cols, dtype,
+                             _stream(stream)))
+
+
+def _ws(workspace) -> tuple[int, int]:
+    return _dev(workspace, "workspace"), workspace.numel() * workspace.element_size()
 
 
 def wisp_verify(model: wisp_model, kv: KVPool, desc: BatchDesc, tokens, draft_probs, rng_seed: int,
                 accept_len, out_tokens, target_logits, workspace, stream=None):
-    _ok(lib.wisp_verify(C.byref(model), C.byref(kv.c), C.byref(desc.c), _ptr(tokens), _ptr(draft_probs),
-                        rng_seed & ((1 << 64) - 1), _ptr(accept_len), _ptr(out_tokens), _ptr(target_logits),
-                        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+    _check_desc(desc)
+    _check_kv(model, kv, model.n_layers)
+    V = model.vocab
+    probs = _dev(draft_probs, "draft_probs", desc.S * V, dtype=_f32()) if desc.S > 0 else _ptr(draft_probs)
+    logits = None if target_logits is None else _dev(target_logits, "target_logits", desc.M * V, dtype=_f32())
+    _ok(lib.wisp_verify(C.byref(model), C.byref(kv.c), C.byref(desc.c),
+                        _dev(tokens, "tokens", desc.rows, dtype=_i32()), probs, rng_seed & ((1 << 64) - 1),
+                        _dev(accept_len, "accept_len", desc.B, dtype=_i32()),
+                        _dev(out_tokens, "out_tokens", desc.M, dtype=_i32()), logits, *_ws(workspace),
+                        _stream(stream)))
 
 
 def wisp_accept(desc: BatchDesc, vocab: int, logits, tokens, draft_probs, rng_seed: int, accept_len,
                 out_tokens, workspace, stream=None):
-    _ok(lib.wisp_accept(C.byref(desc.c), vocab, _ptr(logits), _ptr(tokens), _ptr(draft_probs),
-                        rng_seed & ((1 << 64) - 1), _ptr(accept_len), _ptr(out_tokens), _ptr(workspace),
-                        workspace.numel() * workspace.element_size(), _stream(stream)))
+    probs = _dev(draft_probs, "draft_probs", desc.S * vocab, dtype=_f32()) if desc.S > 0 else _ptr(draft_probs)
+    _ok(lib.wisp_accept(C.byref(desc.c), vocab, _dev(logits, "logits", desc.M * max(vocab, 0), dtype=_f32()),
+                        _dev(tokens, "tokens", desc.M, dtype=_i32()), probs, rng_seed & ((1 << 64) - 1),
+                        _dev(accept_len, "accept_len", desc.B, dtype=_i32()),
+                        _dev(out_tokens, "out_tokens", desc.M, dtype=_i32()), *_ws(workspace), _stream(stream)))
 
 
 def wisp_attention(model: wisp_model, kv: KVPool, desc: BatchDesc, q, out, workspace, stream=None):
-    _ok(lib.wisp_attention(C.byref(model), C.byref(kv.c), C.byref(desc.c), _ptr(q), _ptr(out),
-                           _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+    _check_desc(desc)
+    _check_kv(model, kv, 1)
+    es = 2 if model.dtype == WISP_BF16 else 4
+    n = desc.rows * model.n_q_heads * model.head_dim
+    _ok(lib.wisp_attention(C.byref(model), C.byref(kv.c), C.byref(desc.c), _dev(q, "q", n, elem=es),
+                           _dev(out, "out", n, elem=es), *_ws(workspace), _stream(stream)))
 
 
 def wisp_uniform(rng_seed: int, req_id: int, tag: int, row: int, n: int, out, stream=None):
-    _ok(lib.wisp_uniform(rng_seed & ((1 << 64) - 1), req_id, tag, row, n, _ptr(out), _stream(stream)))
+    _ok(lib.wisp_uniform(rng_seed & ((1 << 64) - 1), req_id, tag, row, n, _dev(out, "out", n, dtype=_f32()),
+                         _stream(stream)))
 
 
 def wisp_schedule(policy: int, requests, t_now: float, mem_budget: float, guard: float, model) -> list:
@@ -387,10 +452,12 @@ def wisp_draft_stats(logits, vocab: int, temperature: float, stats, ws=None, str
     `ws` (a device byte tensor of wisp_draft_stats_workspace_size bytes) is allocated when
     not given."""
     rows = logits.shape[0]
+    if logits.dim() != 2 or logits.stride(1) != 1 or logits.shape[1] < vocab:
+        raise ValueError(f"logits: expected [rows][>= {vocab}] with unit column stride")
     if ws is None:
         ws = workspace(lib.wisp_draft_stats_workspace_size(rows, vocab))
-    _ok(lib.wisp_draft_stats(_ptr(logits), rows, vocab, logits.stride(0), temperature, _ptr(stats), _ptr(ws),
-                             ws.numel(), _stream(stream)))
+    _ok(lib.wisp_draft_stats(_dev(logits, "logits", dtype=_f32(), contiguous=False), rows, vocab, logits.stride(0),
+                             temperature, _dev(stats, "stats", rows * 4, dtype=_f32()), *_ws(ws), _stream(stream)))
 
 
 class RejectMLP:
@@ -400,13 +467,16 @@ class RejectMLP:
 
     def __init__(self, params: dict):
         self.t = {k: v.contiguous() for k, v in params.items() if k != "b4"}
+        for k, v in self.t.items():
+            _dev(v, f"params[{k!r}]", dtype=_f32())
         self.c = wisp_reject_mlp(int(self.t["w1"].shape[1]), *[self.t[k].data_ptr() for k in
                                  ("mean", "inv_std", "w1", "b1", "w2", "b2", "w3", "b3", "w4")], float(params["b4"]))
 
 
 def wisp_reject_predict(mlp: RejectMLP, features, p_accept, stream=None):
-    _ok(lib.wisp_reject_predict(C.byref(mlp.c), _ptr(features), features.shape[0], _ptr(p_accept),
-                                _stream(stream)))
+    rows = features.shape[0]
+    _ok(lib.wisp_reject_predict(C.byref(mlp.c), _dev(features, "features", rows * mlp.c.n_in, dtype=_f32()), rows,
+                                _dev(p_accept, "p_accept", rows, dtype=_f32()), _stream(stream)))
 
 
 class KVManager:
@@ -473,7 +543,7 @@ class KVManager:
 
 
 def wisp_check(workspace, stream=None):
-    _ok(lib.wisp_check(_ptr(workspace), _stream(stream)))
+    _ok(lib.wisp_check(_dev(workspace, "workspace"), _stream(stream)))
 
 
 def workspace(nbytes: int, device="cuda"):

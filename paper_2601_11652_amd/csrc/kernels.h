@@ -84,6 +84,7 @@ struct AttnGroup {  // the chunks of one (request, kv head, row group), combined
 };
 constexpr int kAttnRowsPerItem = 48;   // query rows one wave carries (3 blocks of 16)
 constexpr int kAttnMaxItems = 1 << 22;  // split-KV work items of one call (int indices, workspace)
+constexpr int kAcceptRowsMax = 1 << 29; // rows of one acceptance-only call (int offsets)
 constexpr int kAttnMaxChunkPages = 64; // pages of one item (one block id per lane)
 
 // split-KV partials of every item, then their fixed-order combine into `out`

@@ -106,9 +106,12 @@ wisp_status check_desc(const wisp_batch_desc *d, bool need_pages, bool forward) 
     if (need_pages && (int64_t)d->pt_stride * WISP_PAGE < need)
       return fail(WISP_E_CAPACITY, "request %d needs %lld tokens but the page table holds %d", i,
                   (long long)need, d->pt_stride * WISP_PAGE);
+    // the model's rows are bounded by WISP_ROWS_MAX; the acceptance alone only by int range
     rows += (forward ? pre : 0) + d->gamma[i] + 1;
-    if (rows > WISP_ROWS_MAX)
-      return fail(WISP_E_UNSUPPORTED, "the batch has more than %d rows (prompt, root and draft rows)", WISP_ROWS_MAX);
+    const int64_t max_rows = forward ? WISP_ROWS_MAX : kAcceptRowsMax;
+    if (rows > max_rows)
+      return fail(WISP_E_UNSUPPORTED, "the batch has more than %lld rows (prompt, root and draft rows)",
+                  (long long)max_rows);
   }
   if (need_pages && !d->kv_page_table) return fail(WISP_E_INVALID, "kv_page_table is NULL");
   return WISP_OK;

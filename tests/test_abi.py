@@ -113,15 +113,16 @@ def test_batch_size_limits(W):
     assert W.wisp_logits_workspace_size(m, over) == 0
     assert _verify(W, m, over) == W.WISP_E_UNSUPPORTED
     assert "rows" in W.wisp_last_error()
-    # the acceptance stage ignores prompt rows
+    # the acceptance stage ignores prompt rows, and takes more rows than the model
     assert W.wisp_accept_workspace_size(over, 1024) > 0
-    # exactly ROWS_MAX rows pass, one more does not (drafts only)
+    # exactly ROWS_MAX forwarded rows pass, one more does not (drafts only)
     B = W.ROWS_MAX // (W.GAMMA_MAX + 1)
     tail = W.ROWS_MAX - B * (W.GAMMA_MAX + 1)
     gam = [W.GAMMA_MAX] * B + ([tail - 1] if tail else [])
     assert sum(g + 1 for g in gam) == W.ROWS_MAX
-    assert W.wisp_accept_workspace_size(_desc(W, [0] * len(gam), gam), 1024) > 0
-    assert W.wisp_accept_workspace_size(_desc(W, [0] * (len(gam) + 1), gam + [0]), 1024) == 0
+    assert W.wisp_workspace_size(m, _desc(W, [0] * len(gam), gam)) > 0
+    assert W.wisp_workspace_size(m, _desc(W, [0] * (len(gam) + 1), gam + [0])) == 0
+    assert W.wisp_accept_workspace_size(_desc(W, [0] * (len(gam) + 1), gam + [0]), 8) > 0
     # contexts whose split-KV work list would pass 2^22 items (bf16 path: 1024 tokens
     # per item at most, one item list per kv head and 48-row group)
     mb = _model(W, dtype=W.WISP_BF16)
@@ -162,3 +163,24 @@ def test_logits_in_workspace_sizes(W):
     args = (C.byref(m), C.byref(kv), C.byref(d.c), FAKE, FAKE, 1, FAKE, FAKE, None, FAKE)
     assert L.wisp_verify(*args, base, None) == W.WISP_E_WORKSPACE
     assert L.wisp_verify(*args, base + W.wisp_logits_workspace_size(m, d) - 1, None) == W.WISP_E_WORKSPACE
+
+
+def test_binding_rejects_host_and_mistyped_tensors(W):
+    """The binding hands the library device pointers only: a host tensor, a wrong element
+    type or too few elements raise before any call (no GPU needed to see it)."""
+    import torch
+    with pytest.raises(ValueError, match="device tensor"):
+        W.wisp_uniform(1, 0, 1, 0, 4, torch.zeros(4))
+    with pytest.raises(ValueError, match="device tensor"):
+        W.wisp_check(torch.zeros(256, dtype=torch.uint8))
+    desc = W.BatchDesc([10], [2], torch.zeros((1, 4), dtype=torch.int32))
+    m = _model(W)
+    kv = W.KVPool(torch.zeros((2, 4, 4, 16 * 64)), torch.zeros((2, 4, 4, 16 * 64)))
+    with pytest.raises(ValueError, match="page_table"):
+        W.wisp_verify(m, kv, desc, None, None, 1, None, None, None, torch.zeros(256, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="device tensor"):
+        W.wisp_accept(desc, 8, torch.zeros((3, 8)), torch.zeros(3, dtype=torch.int32), torch.zeros((2, 8)), 1,
+                      torch.zeros(1, dtype=torch.int32), torch.zeros(3, dtype=torch.int32),
+                      torch.zeros(256, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="unit column stride"):
+        W.wisp_draft_stats(torch.zeros((8, 4)).t(), 8, 1.0, torch.zeros((4, 4)))
