@@ -66,8 +66,8 @@ typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
  *   w_gate_up[l] rows 2 * d_ff (W_gate rows, then W_up), K = d_model
  *   w_down[l]   rows d_model,   K = d_ff
  *   lm_head     rows vocab,     K = d_model
- * Shapes: d_model and d_ff multiples of 32, d_model <= 8192; head_dim a multiple of 32
- * (64 or 128 for WISP_BF16), n_q_heads a multiple of n_kv_heads; for WISP_BF16 also vocab a
+ * Shapes: d_model and d_ff multiples of 32, d_model <= 8192; head_dim a multiple of 32 up
+ * to 256 (64 or 128 for WISP_BF16), n_q_heads a multiple of n_kv_heads; for WISP_BF16 also vocab a
  * multiple of 32 and at most 64 query heads per kv head.  Others: WISP_E_UNSUPPORTED.
  * Linear weights ("rows x K", nn.Linear's [out][in]) must be stored in the packed
  * form made by wisp_pack_linear(): for WISP_BF16 an MFMA-fragment order, for

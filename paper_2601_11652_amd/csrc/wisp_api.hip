@@ -65,7 +65,8 @@ wisp_status check_model(const wisp_model *m, bool need_weights) {
     return fail(WISP_E_INVALID, "model dimensions must be positive");
   if (m->dtype != WISP_F32 && m->dtype != WISP_BF16) return fail(WISP_E_UNSUPPORTED, "dtype %d", m->dtype);
   if (m->n_q_heads % m->n_kv_heads) return fail(WISP_E_UNSUPPORTED, "n_q_heads %% n_kv_heads != 0");
-  if (m->head_dim % 32) return fail(WISP_E_UNSUPPORTED, "head_dim must be a multiple of 32");
+  if (m->head_dim % 32 || m->head_dim > 256)
+    return fail(WISP_E_UNSUPPORTED, "head_dim must be a multiple of 32, at most 256");
   if (m->d_model % 32 || m->d_ff % 32) return fail(WISP_E_UNSUPPORTED, "d_model, d_ff must be multiples of 32");
   // the residual + norm kernels hold a row in one workgroup, 8 columns per thread
   if (m->d_model > 8192) return fail(WISP_E_UNSUPPORTED, "d_model > 8192");

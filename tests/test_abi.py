@@ -79,6 +79,7 @@ def test_validation_statuses(W):
     assert _verify(W, _model(W, embed=None), _desc(W, [10], [2])) == W.WISP_E_INVALID
     assert _verify(W, _model(W, d_model=8192 + 32), _desc(W, [10], [2])) == W.WISP_E_UNSUPPORTED
     assert "d_model" in W.wisp_last_error()
+    assert _verify(W, _model(W, head_dim=288, n_q_heads=1, n_kv_heads=1), _desc(W, [10], [2])) == W.WISP_E_UNSUPPORTED
     assert W.wisp_workspace_size(_model(W, d_model=8192), _desc(W, [10], [2])) > 0
     L = W.load_library()
     assert L.wisp_verify(None, None, None, None, None, 0, None, None, None, None, 0, None) == W.WISP_E_INVALID
