@@ -77,3 +77,26 @@ def test_attention_matches_oracle(ctx, gamma, n_q, n_kv, hd, bf16):
         assert err.mean() < 3e-3, err.mean()
     else:
         assert err.max() < 1e-5, err.max()
+
+
+def test_fp32_attention_at_its_longest_context():
+    """The fp32 path keeps a request's scores in dynamic LDS (4 bytes per token): at the
+    documented maximum of 32768 tokens per request that is 128 KB in one workgroup."""
+    ctx, gamma = [32768 - 5], [4]
+    log(f"fp32 attention at {ctx[0] + gamma[0] + 1} tokens")
+    ctx, gamma, pt, kp, vp, q = _case(ctx, gamma, 4, 2, 32, False, seed=32768)
+    shape = wi.ModelShape("attn", 1, 128, 4, 2, 32, 128, 256, "f32", 1e4)
+    model = W.GpuModel.shape_only(shape)
+    kv = W.KVPool(to_dev(kp[None]), to_dev(vp[None]))
+    desc = W.BatchDesc(ctx, gamma, to_dev(pt), 1.0)
+    ws = W.workspace(W.wisp_workspace_size(model, desc))
+    dq = to_dev(q)
+    out = torch.zeros_like(dq)
+    W.wisp_attention(model, kv, desc, dq, out, ws)
+    W.wisp_check(ws)
+    want = oracle.paged_attention(q.astype(np.float64), kp, vp, pt, ctx, gamma + 1, 2, False)
+    got = out.cpu().numpy().astype(np.float64)
+    # each output sums 32768 fp32 products in order: relative bar of the fp32 path
+    rel = np.abs(got - want).max() / np.abs(want).max()
+    log(f"  max relative error {rel:.2e}")
+    assert rel < 1e-4, rel
