@@ -21,9 +21,10 @@ Pins (tests/test_oracle_*.py): a hand-worked acceptance example, closed forms
 (q = p accepts everything, gamma = 0 is plain decoding, T = 0 is greedy), chi-square
 tests of the output law on V = 8, the acceptance-length law P(L >= k) = alpha^k,
 a negative control (the literal "extra token ~ p" reading must fail), an fp64 dense
-brute-force attention, Philox known-answer vectors, and forward invariants.
-The end-to-end forward logits of a random-init model have no external value to
-match: beyond those invariants they are "parity unpinned".
+brute-force attention, Philox known-answer vectors, forward invariants, and a dense
+fp64 reformulation of the forward from torch library routines (rms_norm, linear,
+complex-rotation RoPE, scaled_dot_product_attention, silu), compared logit by logit.
+The weights are random-init, so no external reference logits exist to match.
 """
 from __future__ import annotations
 
