@@ -12,7 +12,6 @@ from scipy import stats
 
 import oracle
 import paper_2601_11652_amd as W
-import wisp_inputs as wi
 from gpu_harness import compare_decisions, log
 
 pytestmark = pytest.mark.gpu

@@ -9,7 +9,6 @@ import numpy as np
 import pytest
 
 import oracle
-import wisp_inputs as wi
 
 P4 = np.array([0.5, 0.25, 0.125, 0.125])
 Q4 = np.array([0.25, 0.5, 0.125, 0.125])
