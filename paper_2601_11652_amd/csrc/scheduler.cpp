@@ -82,7 +82,7 @@ extern "C" wisp_status wisp_schedule(int32_t policy, const wisp_sched_request *q
     *batch_len = 0;
     if (n == 0) return WISP_OK;
     std::vector<char> expired(n, 0);
-    Batch b{q, *model, t_now, mem_budget, expired};
+    Batch b{q, *model, t_now, mem_budget, expired, {}};
 
     if (policy == WISP_SCHED_FCFS) {
       std::vector<int32_t> order(n);

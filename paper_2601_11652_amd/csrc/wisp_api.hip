@@ -119,7 +119,7 @@ wisp_status check_desc(const wisp_batch_desc *d, bool need_pages, bool forward) 
   return WISP_OK;
 }
 
-void carve(Plan &p, size_t &w, size_t &field, size_t bytes) {
+void carve(size_t &w, size_t &field, size_t bytes) {
   field = w;
   w = align256(w + bytes);
 }
@@ -276,24 +276,24 @@ wisp_status make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bo
 
   // workspace
   size_t w = 0;
-  carve(p, w, p.w_err, 256);
-  carve(p, w, p.w_desc, p.host.size() * sizeof(int32_t));
+  carve(w, p.w_err, 256);
+  carve(w, p.w_desc, p.host.size() * sizeof(int32_t));
   const int CH = sampler_chunks(std::max(p.V, 1));
-  carve(p, w, p.w_sm, (size_t)p.Mv * CH * 4);
-  carve(p, w, p.w_si, (size_t)p.Mv * CH * 4);
-  carve(p, w, p.w_ss, (size_t)p.Mv * CH * 8);
-  carve(p, w, p.w_vtok, (size_t)(p.prefill ? p.Mv : 0) * 4);
-  carve(p, w, p.w_rk, (size_t)p.B * CH * 2 * 4);
-  carve(p, w, p.w_ri, (size_t)p.B * CH * 2 * 4);
-  carve(p, w, p.w_rR, (size_t)p.B * 4);
+  carve(w, p.w_sm, (size_t)p.Mv * CH * 4);
+  carve(w, p.w_si, (size_t)p.Mv * CH * 4);
+  carve(w, p.w_ss, (size_t)p.Mv * CH * 8);
+  carve(w, p.w_vtok, (size_t)(p.prefill ? p.Mv : 0) * 4);
+  carve(w, p.w_rk, (size_t)p.B * CH * 2 * 4);
+  carve(w, p.w_ri, (size_t)p.B * CH * 2 * 4);
+  carve(w, p.w_rR, (size_t)p.B * 4);
   if (forward) {
     const size_t es = p.bf16 ? 2 : 4;
-    carve(p, w, p.w_rope, (size_t)p.M * p.hd * 4);
-    carve(p, w, p.w_h, (size_t)p.M * p.d * 4);
-    carve(p, w, p.w_xn, (size_t)p.Mp * p.d * es);
-    carve(p, w, p.w_ao, (size_t)p.Mp * p.qdim * es);
-    carve(p, w, p.w_af, (size_t)p.Mp * p.F * es);
-    carve(p, w, p.w_q, (size_t)p.M * p.qdim * es);
+    carve(w, p.w_rope, (size_t)p.M * p.hd * 4);
+    carve(w, p.w_h, (size_t)p.M * p.d * 4);
+    carve(w, p.w_xn, (size_t)p.Mp * p.d * es);
+    carve(w, p.w_ao, (size_t)p.Mp * p.qdim * es);
+    carve(w, p.w_af, (size_t)p.Mp * p.F * es);
+    carve(w, p.w_q, (size_t)p.M * p.qdim * es);
     size_t part = 0;
     if (p.bf16) {
       part = std::max({(size_t)p.g_qkv.splits * p.qkvN, (size_t)p.g_o.splits * p.d,
@@ -301,9 +301,9 @@ wisp_status make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bo
     } else {
       part = std::max({(size_t)p.qkvN, (size_t)p.d, (size_t)2 * p.F});
     }
-    carve(p, w, p.w_part, part * p.M * 4);
-    carve(p, w, p.w_attn_o, p.items.size() * (size_t)p.hd * 64 * 4);
-    carve(p, w, p.w_attn_ml, p.items.size() * 64 * 2 * 4);
+    carve(w, p.w_part, part * p.M * 4);
+    carve(w, p.w_attn_o, p.items.size() * (size_t)p.hd * 64 * 4);
+    carve(w, p.w_attn_ml, p.items.size() * 64 * 2 * 4);
   }
   p.total = w;
   return WISP_OK;
