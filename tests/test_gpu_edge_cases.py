@@ -13,7 +13,10 @@
   odd number of 32-row fragments (150 rows: one half carries a zero fragment) and an even
   one (192 rows);
 * an out-of-range block id in the page table: the kernels clamp it, write nothing through
-  it, and wisp_check reports a device input error.
+  it, and wisp_check reports a device input error;
+* a bf16 model of odd widths: d_model 96, d_ff 160, 3 query heads on 1 kv head, vocabulary
+  1056.  Every projection then has a partly filled last column tile and a K shorter than
+  one weight ring, and the GQA group is not a power of two.
 """
 import numpy as np
 import pytest
@@ -190,3 +193,10 @@ def test_logits_kept_in_the_workspace():
     W.wisp_check(ws)
     torch.cuda.synchronize()
     assert np.array_equal(acc.cpu().numpy(), acc_a) and np.array_equal(out.cpu().numpy(), out_a)
+
+
+ODD_BF16 = wi.ModelShape("odd-bf16", 2, 96, 3, 1, 64, 160, 1056, "bf16", 10000.0)
+
+
+def test_odd_widths_bf16():
+    _run_case(ODD_BF16, [0, 37, 200, 5, 1], [16, 3, 0, 9, 1], _bf16_abs, 6e-2)
