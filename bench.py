@@ -236,7 +236,9 @@ def sweep(args, W, wi, gm):
         print(json.dumps(row), flush=True)
     if args.sweep_out:
         with open(args.sweep_out, "w") as f:
-            json.dump({"config": args.config, "steps": args.steps, "warmup": args.warmup, "rows": rows}, f, indent=1)
+            from paper_2601_11652_amd.records import command_line
+            json.dump({"config": args.config, "steps": args.steps, "warmup": args.warmup, "rows": rows,
+                       "command": command_line(None)}, f, indent=1)
 
 
 def main():

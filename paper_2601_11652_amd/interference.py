@@ -24,6 +24,7 @@ import sys
 import time
 
 import numpy as np
+from .records import command_line
 
 PAGE = 16
 
@@ -108,6 +109,7 @@ def main(argv=None):
            "seconds": time.time() - t0}
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     with open(args.out, "w") as f:
+        rec["command"] = command_line("paper_2601_11652_amd.interference", argv)
         json.dump(rec, f, indent=1)
 
 

@@ -24,6 +24,7 @@ import json
 from dataclasses import dataclass, asdict
 
 import numpy as np
+from .records import command_line
 
 FEATURES = ("N_linear", "N_interactions", "N_cached")
 
@@ -235,6 +236,7 @@ def main(argv=None):
                   f"max err {1e3 * t['test']['max_err']:.2f} ms{extra}")
     if args.out:
         with open(args.out, "w") as f:
+            rec["command"] = command_line("paper_2601_11652_amd.latency_model", argv)
             json.dump(rec, f, indent=1)
 
 

@@ -46,6 +46,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from .latency_model import fit_report, step_features
+from .records import command_line
 
 PAGE = 16
 DRAFTS = 5
@@ -257,6 +258,7 @@ def main(argv=None):
         rec = replay(args.replay, shape, log=lambda m: print(m, flush=True))
         rec["seconds"] = time.time() - t0
         with open(args.out, "w") as f:
+            rec["command"] = command_line("paper_2601_11652_amd.latency_sweep", argv)
             json.dump(rec, f, indent=1)
         print(json.dumps({k: rec[k] for k in ("n", "mape_pct", "mean_rel_err_pct", "p90_abs_rel_err_pct",
                                                "ms_range")}), flush=True)
@@ -289,6 +291,7 @@ def main(argv=None):
         summary["appc_fit_on_serving_range"] = rec["appc_fit_on_serving_range"]
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     with open(args.out, "w") as f:
+        rec["command"] = command_line("paper_2601_11652_amd.latency_sweep", argv)
         json.dump(rec, f, indent=1)
     print(json.dumps(summary), flush=True)
 

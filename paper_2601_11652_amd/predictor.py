@@ -25,6 +25,7 @@ import sys
 import numpy as np
 
 from . import RejectMLP, wisp_draft_stats, wisp_reject_predict
+from .records import command_line
 
 HBM_PEAK_GBS = 8000.0
 
@@ -223,6 +224,7 @@ def main(argv=None):
             rec[name] = controller_experiment(shape, gm, log=lambda m: print(m, flush=True), **kw)
         os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
         with open(args.out, "w") as f:
+            rec["command"] = command_line("paper_2601_11652_amd.predictor", argv)
             json.dump(rec, f, indent=1)
         return
     rec = {"stats": [], "mlp": []}
@@ -237,6 +239,7 @@ def main(argv=None):
         print(f"reject_mlp {rows:5d} rows: {r['us']:8.2f} us ({r['TFLOPs']:.2f} TFLOP/s)", flush=True)
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     with open(args.out, "w") as f:
+        rec["command"] = command_line("paper_2601_11652_amd.predictor", argv)
         json.dump(rec, f, indent=1)
 
 

@@ -33,6 +33,7 @@ import numpy as np
 
 from . import (PAGE, BatchDesc, KVManager, KVPool, wisp_draft_stats, wisp_reject_predict, wisp_verify,
                wisp_workspace_size, workspace)
+from .records import command_line
 
 
 class Sessions:
@@ -358,6 +359,7 @@ def main(argv=None):
     res["seconds"] = time.time() - t0
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     with open(args.out, "w") as f:
+        res["command"] = command_line("paper_2601_11652_amd.sessions", argv)
         json.dump(res, f)
     for name, e in res["experiments"].items():
         s = e["summary"]

@@ -45,6 +45,7 @@ import time
 import numpy as np
 
 from . import WISP_SCHED_FCFS, WISP_SCHED_SLO, WISP_SCHED_SLO_LIVE, lib, wisp_latency_model, wisp_sched_request, _ok
+from .records import command_line
 
 CLASSES = (2.0, 4.0, 6.0, 8.0)
 RESPONSE_TOKENS = 128
@@ -515,6 +516,7 @@ def main(argv=None):
     rec["replay_n"] = args.replay_n
     os.makedirs(os.path.dirname(args.out) or ".", exist_ok=True)
     with open(args.out, "w") as f:
+        rec["command"] = command_line("paper_2601_11652_amd.slo_sim", argv)
         json.dump(rec, f)
     print(json.dumps(rec["capacity"]), flush=True)
 
