@@ -246,11 +246,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
   const int n = g.n_items;
   auto item_of = [&](int c) { return (int64_t)g.first_item + min(c, n - 1); };   // clamped, in range
 
+  // a group's threads fill whole waves (UNITS is a multiple of 64), so `cb + c < n` is
+  // wave-uniform: chunks past the group's last are not loaded at all
   float m = -INFINITY;
   for (int cb = 0; cb < n; cb += MAXC) {
     float mc[MAXC];
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c) mc[c] = part_ml[(item_of(cb + c) * 64 + rr) * 2];
+    for (int c = 0; c < MAXC; ++c) mc[c] = cb + c < n ? part_ml[(item_of(cb + c) * 64 + rr) * 2] : -INFINITY;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c)
       if (cb + c < n) m = fmaxf(m, mc[c]);
@@ -261,12 +263,18 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
     float mc[MAXC], lc[MAXC], pv[MAXC][8];
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
-      const int64_t itm = item_of(cb + c);
-      mc[c] = part_ml[(itm * 64 + rr) * 2];
-      lc[c] = part_ml[(itm * 64 + rr) * 2 + 1];
-      const float *po = part_o + (itm * HD + c0) * 64 + rr;
+      mc[c] = -INFINITY;
+      lc[c] = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pv[c][e] = po[e * 64];
+      for (int e = 0; e < 8; ++e) pv[c][e] = 0.f;
+      if (cb + c < n) {
+        const int64_t itm = item_of(cb + c);
+        mc[c] = part_ml[(itm * 64 + rr) * 2];
+        lc[c] = part_ml[(itm * 64 + rr) * 2 + 1];
+        const float *po = part_o + (itm * HD + c0) * 64 + rr;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pv[c][e] = po[e * 64];
+      }
     }
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
