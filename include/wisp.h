@@ -224,7 +224,9 @@ wisp_status wisp_check(void *workspace, void *stream);
  *   ATTN: K and V bytes of every token each kv head reads (ctx_len + gamma + 1 per request);
  *   SAMPLER: two passes over the fp32 logits plus one row per request;
  *   ATTN_COMBINE, ROWS: none (overhead kernels).
- * wisp_profile_read synchronises on the recorded events.
+ * wisp_profile_read synchronises on the recorded events.  The profiling state is one per
+ * process: enable, read and reset it from one thread, while no other thread calls the
+ * library.
  */
 #define WISP_PROF_GEMM_RING1 0   /* gemm_ring_kernel, one 32-column fragment per wave (4 or 8 waves) */
 #define WISP_PROF_GEMM_RING2 1   /* gemm_ring_kernel, two 32-column fragments per wave  */
