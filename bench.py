@@ -94,10 +94,12 @@ def traffic_from_counters(kernel_key: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(mix, sample_req: int):
-    """The CPU oracle on one request of the same workload (same weights, context KV, root
-    token and gamma; its drafts come from the oracle's own fixture).  Times the oracle's
-    verification of that request: forward of its gamma+1 rows plus acceptance."""
+def cpu_baseline(mix, order, min_seconds: float = 10.0):
+    """The CPU oracle on a bounded sample of the same workload: requests of the batch in the
+    given order (same weights, context KV, root token and gamma; their drafts come from the
+    oracle's own fixture) until at least min_seconds of oracle time are spent.  Times the
+    oracle's verification of each sampled request, i.e. the forward of its gamma+1 rows
+    plus acceptance; the rate is the sample's committed tokens over that time."""
     import numpy as np
     import oracle
     import wisp_inputs as wi
@@ -106,27 +108,39 @@ def cpu_baseline(mix, sample_req: int):
     t0 = time.time()
     model = fx.host_model(s, mix.seed)
     log(f"cpu baseline: host weights generated in {time.time() - t0:.1f} s")
-    i = sample_req
-    sub = wi.custom_mix(s, [mix.ctx_len[i]], [mix.gamma[i]], seed=mix.seed, name=mix.config)
-    sub.t_draft[:] = mix.t_draft[i]
-    sub.sigma[:] = mix.sigma[i]
-    n_pages = (int(mix.ctx_len[i]) + int(mix.gamma[i]) + 1 + 15) // 16
-    pt = np.arange(n_pages, dtype=np.int32)[None, :]
-    pools = fx.empty_pools(s, n_pages)
-    fx.place_synthetic_kv(sub, pools, pt, req_keys=[i])
-    roots = wi.root_tokens(mix)[i:i + 1]
-    work = (pools[0].copy(), pools[1].copy())
-    toks, qs, _ = fx.draft_fixture(model, sub, work, pt, roots)
-    t1 = time.time()
-    logits = oracle.forward(model, pools[0], pools[1], pt, sub.ctx_len, sub.rows, toks[0])
-    res = oracle.accept(logits, toks[0], qs[0], sub.gamma, 1.0, wi.verify_seed(mix), req_id=[i])
-    dt = time.time() - t1
-    committed = int(res.accept_len[0]) + 1
+    roots_all = wi.root_tokens(mix)
+    dt = 0.0
+    committed = 0
+    done = []
+    for i in order:
+        i = int(i)
+        sub = wi.custom_mix(s, [mix.ctx_len[i]], [mix.gamma[i]], seed=mix.seed, name=mix.config)
+        sub.t_draft[:] = mix.t_draft[i]
+        sub.sigma[:] = mix.sigma[i]
+        n_pages = (int(mix.ctx_len[i]) + int(mix.gamma[i]) + 1 + 15) // 16
+        pt = np.arange(n_pages, dtype=np.int32)[None, :]
+        pools = fx.empty_pools(s, n_pages)
+        fx.place_synthetic_kv(sub, pools, pt, req_keys=[i])
+        work = (pools[0].copy(), pools[1].copy())
+        toks, qs, _ = fx.draft_fixture(model, sub, work, pt, roots_all[i:i + 1])
+        t1 = time.time()
+        logits = oracle.forward(model, pools[0], pools[1], pt, sub.ctx_len, sub.rows, toks[0])
+        res = oracle.accept(logits, toks[0], qs[0], sub.gamma, 1.0, wi.verify_seed(mix), req_id=[i])
+        dt += time.time() - t1
+        committed += int(res.accept_len[0]) + 1
+        done.append(i)
+        log(f"cpu baseline: request {i} (ctx {int(mix.ctx_len[i])}, gamma {int(mix.gamma[i])}), "
+            f"{dt:.1f} s of oracle time so far")
+        if dt >= min_seconds:
+            break
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    ctx = [int(mix.ctx_len[i]) for i in done]
+    gam = [int(mix.gamma[i]) for i in done]
     return {"value": committed / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": (f"request {i} of the {mix.config} batch (ctx {int(mix.ctx_len[i])}, gamma "
-                       f"{int(mix.gamma[i])}): forward of its {int(mix.gamma[i]) + 1} rows through all "
-                       f"{s.n_layers} layers plus acceptance, {committed} committed tokens in {dt:.2f} s")}
+            "sample": (f"{len(done)} requests of the {mix.config} batch around its median context "
+                       f"(ctx {min(ctx)}-{max(ctx)}, gamma {min(gam)}-{max(gam)}): forward of their "
+                       f"gamma+1 rows through all {s.n_layers} layers plus acceptance, {committed} "
+                       f"committed tokens in {dt:.2f} s of oracle time")}
 
 
 def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = True):
@@ -327,9 +341,13 @@ def main():
         "kernels": classes,
     }
     if not args.no_cpu_baseline:
-        sample = int(np.argsort(mix.ctx_len)[mix.B // 2])
+        # requests outward from the median context: median, next above, next below, ...
+        by_ctx = np.argsort(mix.ctx_len, kind="stable")
+        mid = mix.B // 2
+        order = [by_ctx[mid + (k + 1) // 2 * (1 if k % 2 else -1)] for k in range(2 * mix.B)
+                 if 0 <= mid + (k + 1) // 2 * (1 if k % 2 else -1) < mix.B]
         try:
-            result["cpu_baseline"] = cpu_baseline(mix, sample)
+            result["cpu_baseline"] = cpu_baseline(mix, order)
         except MemoryError as e:   # report rather than fail the GPU measurement
             result["cpu_baseline"] = {"value": None, "error": str(e)}
     print(json.dumps(result), flush=True)
