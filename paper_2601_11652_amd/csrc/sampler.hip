@@ -145,8 +145,10 @@ __device__ RowStat row_stat(const float *part_m, const int32_t *part_i, const do
   return st;
 }
 
-// pass 3: Eq. (1)-(2) accept scan (recomputed by every chunk's workgroup, <= 16 steps),
-// then that chunk's part of the exponential race for the extra token (Eq. (3) / residual)
+// pass 3: Eq. (1)-(2) acceptance (recomputed by every chunk's workgroup), then that chunk's
+// part of the exponential race for the extra token (Eq. (3) / residual).  The <= 16 draft
+// decisions are independent of one another, so thread j - 1 takes draft j's and R is the
+// smallest rejected j (gamma + 1 when none is): one round of loads instead of a chain.
 __global__ __launch_bounds__(256) void race_kernel(StepDesc d, int V, const float *__restrict__ logits,
                                                    const int32_t *__restrict__ tokens,
                                                    const float *__restrict__ q, float T, uint64_t seed,
@@ -162,36 +164,31 @@ __global__ __launch_bounds__(256) void race_kernel(StepDesc d, int V, const floa
   const int c = blockIdx.y, i = blockIdx.x;
   const int gam = d.gamma[i], off = d.off[i], doff = d.doff[i];
   const uint32_t req = d.req_id[i];
-  if (threadIdx.x == 0) {
-    int R = gam + 1;
-    for (int j = 1; j <= gam; ++j) {
-      int y = tokens[off + j];
-      if (y < 0 || y >= V) {
-        if (c == 0) flag_error(d.err, kErrToken);
-        y = 0;
-      }
-      const int64_t pr = off + j - 1;
-      const RowStat st = row_stat(part_m, part_i, part_s, pr, CH, T);
-      if (T == 0.f) {
-        if (y != st.amax) {
-          R = j;
-          break;
-        }
-      } else {
-        const float P = expf(logits[pr * V + y] / T - st.m) / st.S;
-        const float Q = q[(int64_t)(doff + j - 1) * V + y];
-        const float a = Q > 0.f ? fminf(1.f, P / Q) : (P > 0.f ? 1.f : 0.f);
-        const float u = uniform_from_word(draw(seed, 0u, (uint32_t)j, req, kTagAccept).v[0]);
-        if (!(u <= a)) {
-          R = j;
-          break;
-        }
-      }
+  if (threadIdx.x == 0) R_sh = gam + 1;
+  __syncthreads();
+  const int j = threadIdx.x + 1;   // gamma <= 16 < 256 threads
+  if (j <= gam) {
+    int y = tokens[off + j];
+    if (y < 0 || y >= V) {
+      if (c == 0) flag_error(d.err, kErrToken);
+      y = 0;
     }
-    R_sh = R;
-    if (c == 0) req_R[i] = R;
+    const int64_t pr = off + j - 1;
+    const RowStat st = row_stat(part_m, part_i, part_s, pr, CH, T);
+    bool rejected_j;
+    if (T == 0.f) {
+      rejected_j = y != st.amax;
+    } else {
+      const float P = expf(logits[pr * V + y] / T - st.m) / st.S;
+      const float Q = q[(int64_t)(doff + j - 1) * V + y];
+      const float a = Q > 0.f ? fminf(1.f, P / Q) : (P > 0.f ? 1.f : 0.f);
+      const float u = uniform_from_word(draw(seed, 0u, (uint32_t)j, req, kTagAccept).v[0]);
+      rejected_j = !(u <= a);
+    }
+    if (rejected_j) atomicMin(&R_sh, j);   // integer minimum: the order of arrival does not matter
   }
   __syncthreads();
+  if (c == 0 && threadIdx.x == 0) req_R[i] = R_sh;
   if (T == 0.f) return;
   const int R = R_sh, r = R - 1;
   const int64_t lr = off + r;
