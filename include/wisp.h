@@ -164,7 +164,8 @@ wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t c
  *                 (root .. y_gamma of each request; prompt rows produce none), or NULL: the
  *                 logits then live in the workspace, which must hold
  *                 wisp_workspace_size + wisp_logits_workspace_size bytes
- *   workspace     DEVICE scratch of >= wisp_workspace_size() bytes
+ *   workspace     DEVICE scratch of >= wisp_workspace_size() bytes; its first 256 bytes
+ *                 hold the fault record and must be zero before the first use (wisp_check)
  * KV: K/V of all prefill_len+gamma+1 new positions are written in place (rejected
  * drafts included); the valid prefix afterwards is ctx_len + prefill_len + 1 + L and
  * later calls overwrite the stale slots (rollback by length).  Repeating a call with the same inputs gives
@@ -172,7 +173,8 @@ wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t c
  * argmax_k [score_k - ln(-ln u_k)], ties to the smallest k, score = ln(residual) after
  * a rejection (or z = logits/T when the residual is empty), z after full acceptance.
  * Device-side input faults (token id outside [0, vocab), block id outside
- * [0, n_blocks)) are recorded in the workspace and reported by wisp_check().
+ * [0, n_blocks)) are recorded in the workspace (sticky across calls) and reported by
+ * wisp_check().
  * Batches of more than WISP_ROWS_MAX rows, or whose contexts would need more than 2^22
  * split-KV work items (about 2^22 x 1024 tokens summed over requests, kv heads and
  * 48-row groups), return WISP_E_UNSUPPORTED; the workspace sizes are then 0.
@@ -210,8 +212,11 @@ wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wis
 wisp_status wisp_uniform(uint64_t rng_seed, uint32_t req_id, uint32_t tag, uint32_t row, uint32_t n,
                          float *out, void *stream);
 
-/* Synchronise `stream`, then report (and clear) device-side input faults recorded in
- * `workspace` by the last wisp_verify / wisp_accept on it. */
+/* Synchronise `stream`, then report (and clear) the device-side input faults recorded in
+ * `workspace` since it was last cleared.  The record (the workspace's first 256 bytes) is
+ * sticky: wisp_verify, wisp_accept and wisp_attention only add to it, so faults of several
+ * calls on one workspace are all reported by the next wisp_check.  A new workspace's first
+ * 256 bytes must be zero before its first use (hipMemset after allocation). */
 wisp_status wisp_check(void *workspace, void *stream);
 
 /*
@@ -239,6 +244,16 @@ wisp_status wisp_check(void *workspace, void *stream);
 wisp_status wisp_profile_enable(int on);
 wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops);
 wisp_status wisp_profile_reset(void);
+
+/*
+ * Launch plan of one bf16 projection of the step (host only; introspection for tests and
+ * benchmarks): M rows, N output columns, K inputs.  out[0] = kernel variant (1: 32-column
+ * weight ring, 2: 64-column weight ring, 3: 32-column weight ring with two waves per SIMD),
+ * out[1] = row blocks, out[2] = 32-row fragments per row block, out[3] = K ranges whose
+ * fp32 partial sums are added in fixed order.  WISP_E_INVALID for M, N or K < 1, or N and
+ * K not multiples of 32 and 16.
+ */
+wisp_status wisp_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t out[4]);
 
 /*
  * Verification batch scheduling (Sec. 4.3, Alg. 1), host code.

@@ -5,7 +5,12 @@ baseline leg of ``bench.py`` are the only code allowed to import it; the product
 library (``paper_2601_11652_amd``) never does, and the two share no code.
 
 The arithmetic lives in plain C (``wisp_oracle.c``, fp64 forward / fp32 acceptance)
-and is reached through ctypes.  What each function follows in the paper:
+and is reached through ctypes.  The forward also has an fp32-accumulation mode
+(``acc32``: every sum in fp32, natural index order), a second correct rounding order
+whose distance from the fp64 result measures the bf16 contract's own noise floor.
+KV pools are natural ``[n_layers][n_blocks][n_kv][16][head_dim]`` arrays (slot-major
+pages); the GPU library's page order is a separate interface layout, converted at the
+test boundary.  What each function follows in the paper:
 
 * ``forward``          -- Sec. 4.5, batched one-step verification over a paged,
                           prefix-cached KV (new rows written in place).
@@ -75,12 +80,13 @@ def _declare(L):
                                    _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.orc_plain_decode.argtypes = [C.c_int, _P, C.c_float, C.c_uint64, C.c_uint32, C.c_uint32]
     L.orc_plain_decode.restype = C.c_int32
-    L.orc_paged_attention.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _P, _P, _P, C.c_int,
-                                      C.c_int, _P, _P, _P, _P]
+    L.orc_paged_attention.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _P, _P, _P,
+                                      C.c_int, C.c_int, _P, _P, _P, _P]
     L.orc_forward.argtypes = [_P, _P, _P, C.c_int, C.c_int, _P, _P, _P, C.c_int, _P, _P]
     L.orc_round_bf16_array.argtypes = [_P, _P, C.c_int64]
     L.orc_row_probs.argtypes = [_P, C.c_int, C.c_float, _P]
     L.orc_rope_apply.argtypes = [_P, C.c_int, C.c_int, C.c_double]
+    L.orc_linear_apply.argtypes = [_P, _P, _P, C.c_int, C.c_int, C.c_int, C.c_int]
     L.orc_rmsnorm_apply.argtypes = [_P, _P, C.c_int, C.c_int, C.c_double, C.c_int]
 
 
@@ -199,27 +205,28 @@ def plain_decode(logits_row, temperature: float, seed: int, req_id: int, row: in
 # ------------------------------------------------------------------------------------
 # forward (Sec. 4.5)
 # ------------------------------------------------------------------------------------
-def paged_attention(q, k_pool, v_pool, page_table, ctx_len, n_new, n_kv: int, bf16: bool):
-    """q [M][n_q][hd] float64; pools of ONE layer ([blocks][n_kv][16*hd] pages in the
-    documented K / V page layouts) as float32 or bf16 bits (uint16).  Returns [M][n_q][hd] fp64."""
+def paged_attention(q, k_pool, v_pool, page_table, ctx_len, n_new, n_kv: int, bf16: bool,
+                    acc32: bool = False):
+    """q [M][n_q][hd] float64; pools of ONE layer ([blocks][n_kv][16][hd], slot-major) as
+    float32 or bf16 bits (uint16).  Returns [M][n_q][hd] fp64."""
     q = _c(q, np.float64)
     M, n_q, hd = q.shape
-    assert hd % 32 == 0, "the documented KV page layout needs head_dim % 32 == 0"
     out = np.empty_like(q)
     pt = _c(page_table, np.int32)
     ctx = _c(ctx_len, np.int32)
     nn = _c(n_new, np.int32)
     kp = np.ascontiguousarray(k_pool)
     vp = np.ascontiguousarray(v_pool)
-    lib().orc_paged_attention(n_q, n_kv, hd, int(bf16), _ptr(kp), _ptr(vp), _ptr(pt), pt.shape[1],
-                              ctx.shape[0], _ptr(ctx), _ptr(nn), _ptr(q), _ptr(out))
+    lib().orc_paged_attention(n_q, n_kv, hd, int(bf16), int(acc32), _ptr(kp), _ptr(vp), _ptr(pt),
+                              pt.shape[1], ctx.shape[0], _ptr(ctx), _ptr(nn), _ptr(q), _ptr(out))
     return out
 
 
 class _OrcModel(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d", C.c_int32), ("n_q", C.c_int32),
                 ("n_kv", C.c_int32), ("hd", C.c_int32), ("F", C.c_int32), ("V", C.c_int32),
-                ("bf16", C.c_int32), ("eps", C.c_double), ("rope_base", C.c_double),
+                ("bf16", C.c_int32), ("acc32", C.c_int32), ("eps", C.c_double),
+                ("rope_base", C.c_double),
                 ("embed", C.c_void_p), ("lm_head", C.c_void_p), ("final_norm", C.c_void_p),
                 ("attn_norm", C.POINTER(C.c_void_p)), ("wq", C.POINTER(C.c_void_p)),
                 ("wk", C.POINTER(C.c_void_p)), ("wv", C.POINTER(C.c_void_p)),
@@ -250,7 +257,6 @@ class OracleModel:
     arrays (fp32 model) or bf16 bit patterns (bf16 model)."""
 
     def __init__(self, shape, layers, glob):
-        assert shape.head_dim % 32 == 0, "the documented KV page layout needs head_dim % 32 == 0"
         self.shape = shape
         self.bf16 = shape.dtype == "bf16"
         self._keep = []
@@ -271,16 +277,18 @@ class OracleModel:
         self.embed = _np_storage(glob["embed"])
         self._keep.append(self.embed)
         self.s = _OrcModel(L, s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.d_ff, s.vocab,
-                           int(self.bf16), s.rms_eps, s.rope_base, self.embed.ctypes.data_as(C.c_void_p),
+                           int(self.bf16), 0, s.rms_eps, s.rope_base, self.embed.ctypes.data_as(C.c_void_p),
                            arr(glob["lm_head"]), arr(glob["final_norm"]), vec("attn_norm"),
                            vec("wq"), vec("wk"), vec("wv"), vec("wo"), vec("mlp_norm"),
                            vec("w_gate"), vec("w_up"), vec("w_down"))
 
 
-def forward(model: OracleModel, k_pool, v_pool, page_table, ctx_len, n_new, tokens) -> np.ndarray:
+def forward(model: OracleModel, k_pool, v_pool, page_table, ctx_len, n_new, tokens,
+            acc32: bool = False) -> np.ndarray:
     """Forward the new rows; updates the host pools in place (numpy arrays
-    [n_layers][n_blocks][n_kv][16*hd] in the documented page layouts, float32 or uint16
-    bf16 bits).  Returns fp32 logits [M][V]."""
+    [n_layers][n_blocks][n_kv][16 * hd], each page slot-major, float32 or uint16 bf16
+    bits).  Returns fp32 logits [M][V].  acc32: every sum accumulates in fp32 in natural
+    index order (the fp64 result is the reference; this mode measures the rounding floor)."""
     assert k_pool.flags["C_CONTIGUOUS"] and v_pool.flags["C_CONTIGUOUS"]
     n_blocks = k_pool.shape[1]
     pt = _c(page_table, np.int32)
@@ -290,6 +298,20 @@ def forward(model: OracleModel, k_pool, v_pool, page_table, ctx_len, n_new, toke
     M = int(nn.sum())
     assert tok.shape[0] == M
     logits = np.empty((M, model.shape.vocab), dtype=np.float32)
-    lib().orc_forward(C.byref(model.s), _ptr(k_pool), _ptr(v_pool), n_blocks, ctx.shape[0],
-                      _ptr(ctx), _ptr(nn), _ptr(pt), pt.shape[1], _ptr(tok), _ptr(logits))
+    model.s.acc32 = int(acc32)
+    try:
+        lib().orc_forward(C.byref(model.s), _ptr(k_pool), _ptr(v_pool), n_blocks, ctx.shape[0],
+                          _ptr(ctx), _ptr(nn), _ptr(pt), pt.shape[1], _ptr(tok), _ptr(logits))
+    finally:
+        model.s.acc32 = 0
     return logits
+
+
+def linear_apply(W, x, acc32: bool = False) -> np.ndarray:
+    """y = x W^T exactly as the forward's projections compute it: W [out][in] fp32 values,
+    x [rows][in]; fp64 sums, or fp32 sums in natural k order with acc32."""
+    W = _c(W, np.float32)
+    x = _c(x, np.float64)
+    y = np.empty((x.shape[0], W.shape[0]), np.float64)
+    lib().orc_linear_apply(_ptr(W), _ptr(x), _ptr(y), x.shape[0], x.shape[1], W.shape[0], int(acc32))
+    return y

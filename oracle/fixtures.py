@@ -36,41 +36,30 @@ def _to_storage(t: torch.Tensor, shape: wi.ModelShape) -> np.ndarray:
 
 
 def place_synthetic_kv(mix: wi.Mix, pools, page_table, requests=None, layers=None, req_keys=None):
-    """Write the input generator's synthetic context KV of the given requests into host pools.
+    """Write the input generator's synthetic context KV of the given requests into host pools
+    (slot-major pages: token t of request i at block page_table[i][t // 16], slot t % 16).
     req_keys[i] (default i) is the request index that keys request i's generated values, so a
     request of a large batch can be reproduced on its own."""
     s = mix.shape
-    kp, vp = pools
+    hd = s.head_dim
+    kp = pools[0].reshape(pools[0].shape[:3] + (wi.PAGE, hd))
+    vp = pools[1].reshape(pools[1].shape[:3] + (wi.PAGE, hd))
+    assert np.shares_memory(kp, pools[0]) and np.shares_memory(vp, pools[1]), "pools must be contiguous"
     dt = torch.float32 if s.dtype == "f32" else torch.bfloat16
     reqs = range(mix.B) if requests is None else requests
     lays = range(s.n_layers) if layers is None else layers
-    hd = s.head_dim
-    kidx = wi.k_page_index(hd)
-    vidx = wi.v_page_index(hd)
     for i in reqs:
         n = int(mix.ctx_len[i])
         if n == 0:
             continue
         key = i if req_keys is None else int(req_keys[i])
-        nf = n // wi.PAGE                     # full pages
-        full = page_table[i, :nf]
+        t = np.arange(n)
+        blk = page_table[i, t // wi.PAGE]
+        slot = t % wi.PAGE
         for li, l in enumerate(lays):
             K, V = wi.kv_values(mix.seed, l, key, 0, n, s.n_kv_heads, hd, "cpu", dt)
-            Kn = _to_storage(K, s)
-            Vn = _to_storage(V, s)
-            if nf:
-                # whole pages by axis permutation (the layout's index tables, split into axes):
-                # K (slot s = 8a + 4b + c, dim e = 32f + 8g + h) sits at [f][b][g][a][c][h],
-                # V (slot s = 8a + c, dim e = 16f + h) sits at [f][a][h][c]
-                k = Kn[:nf * wi.PAGE].reshape(nf, 2, 2, 4, s.n_kv_heads, hd // 32, 4, 8)
-                kp[li, full] = k.transpose(0, 4, 5, 2, 6, 1, 3, 7).reshape(nf, s.n_kv_heads, -1)
-                v = Vn[:nf * wi.PAGE].reshape(nf, 2, 8, s.n_kv_heads, hd // 16, 16)
-                vp[li, full] = v.transpose(0, 3, 4, 1, 5, 2).reshape(nf, s.n_kv_heads, -1)
-            if n > nf * wi.PAGE:
-                blk = page_table[i, nf]
-                sl = np.arange(n - nf * wi.PAGE)
-                kp[li, blk][:, kidx[sl]] = Kn[nf * wi.PAGE:].transpose(1, 0, 2)
-                vp[li, blk][:, vidx[sl]] = Vn[nf * wi.PAGE:].transpose(1, 0, 2)
+            kp[li, blk, :, slot] = _to_storage(K, s)          # [n][n_kv][hd]
+            vp[li, blk, :, slot] = _to_storage(V, s)
 
 
 def prefill_context(model: OracleModel, mix: wi.Mix, pools, page_table, requests=None):
@@ -112,30 +101,6 @@ def draft_fixture(model: OracleModel, mix: wi.Mix, pools, page_table, roots, req
     return ({i: np.array(toks[i], np.int32) for i in reqs},
             {i: (np.stack(qs[i]) if qs[i] else np.zeros((0, V), np.float32)) for i in reqs},
             {i: (np.stack(lgs[i]) if lgs[i] else np.zeros((0, V), np.float32)) for i in reqs})
-
-
-class perturbed_embedding:
-    """Context manager: moves embedding entries (token, col) of a host model by one unit in
-    the last place of their storage format, and restores them on exit.  Used to measure how
-    far the model's own rounding noise carries a minimal input change."""
-
-    def __init__(self, model: OracleModel, token: int, cols=(17, 2011)):
-        self.e = model.embed
-        self.token = int(token)
-        self.cols = [c % self.e.shape[1] for c in cols]
-        self.saved = None
-
-    def __enter__(self):
-        self.saved = self.e[self.token, self.cols].copy()
-        if self.e.dtype == np.uint16:
-            self.e[self.token, self.cols] = self.saved + 1          # next bf16 bit pattern
-        else:
-            self.e[self.token, self.cols] = np.nextafter(self.saved, np.float32(np.inf))
-        return self
-
-    def __exit__(self, *exc):
-        self.e[self.token, self.cols] = self.saved
-        return False
 
 
 def random_drafts(mix: wi.Mix, requests, roots, tag: int = 9):

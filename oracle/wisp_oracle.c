@@ -11,6 +11,10 @@
  *     rows' K/V are written in place at positions ctx_len .. ctx_len+gamma.
  *     Arithmetic is fp64; in bf16 mode values are rounded to bf16 at the
  *     points where the GPU path stores bf16 (GEMM inputs, q/k/v, KV pages).
+ *     A second mode (acc32) accumulates every sum in fp32 in natural index
+ *     order instead -- one more correct rounding order, used to measure how far
+ *     two correct accumulation orders drift apart through the bf16 rounding
+ *     points (the floor any other fp32-accumulating implementation lands on).
  *   - acceptance (Sec. 2.4, Eq. (1)-(3), with the residual distribution of
  *     Leviathan et al. that the paper relies on for losslessness): fp32, the
  *     precision in which the GPU path takes the same decisions.
@@ -319,6 +323,7 @@ int32_t orc_plain_decode(int V, const float *l, float T, uint64_t seed, uint32_t
 typedef struct {
   int32_t n_layers, d, n_q, n_kv, hd, F, V;
   int32_t bf16;          /* 0: fp32 storage, no rounding; 1: bf16 storage and rounding     */
+  int32_t acc32;         /* 0: sums in fp64; 1: sums in fp32, natural index order          */
   double eps, rope_base;
   const void *embed;     /* [V][d]                                                       */
   const void *lm_head;   /* [V][d]                                                       */
@@ -333,18 +338,30 @@ static double wval(const orc_model *m, const void *p, int64_t i) {
 
 static double act_round(const orc_model *m, double x) { return m->bf16 ? round_bf16(x) : x; }
 
-/* y[r][n] = sum_k x[r][k] * W[n][k] for all rows r (W natural [out][in] layout). */
+/* y[r][n] = sum_k x[r][k] * W[n][k] for all rows r (W natural [out][in] layout).
+ * acc32: the products of the fp32 operands are summed in fp32, k = 0, 1, ... */
 static void linear(const orc_model *m, const void *W, const double *x, double *y, int rows,
                    int in, int outn) {
 #pragma omp parallel for schedule(static)
   for (int n = 0; n < outn; n++) {
     for (int r = 0; r < rows; r++) {
-      double acc = 0.0;
       const double *xr = x + (int64_t)r * in;
-      for (int k = 0; k < in; k++) acc += xr[k] * wval(m, W, (int64_t)n * in + k);
-      y[(int64_t)r * outn + n] = acc;
+      if (m->acc32) {
+        float acc = 0.0f;
+        for (int k = 0; k < in; k++) acc += (float)xr[k] * (float)wval(m, W, (int64_t)n * in + k);
+        y[(int64_t)r * outn + n] = acc;
+      } else {
+        double acc = 0.0;
+        for (int k = 0; k < in; k++) acc += xr[k] * wval(m, W, (int64_t)n * in + k);
+        y[(int64_t)r * outn + n] = acc;
+      }
     }
   }
+}
+
+/* The residual update h += t; acc32 keeps the residual stream in fp32. */
+static void residual_add(const orc_model *m, double *h, const double *t, int64_t n) {
+  for (int64_t e = 0; e < n; e++) h[e] = m->acc32 ? (double)((float)h[e] + (float)t[e]) : h[e] + t[e];
 }
 
 /* RMSNorm: x * g / sqrt(mean(x^2) + eps). */
@@ -372,11 +389,8 @@ static void rope(double *v, int hd, int pos, double base) {
   }
 }
 
-/* KV page layout for one layer: [n_blocks][n_kv][page], a page holding 16 slots x hd.
- * Inside a page, element (slot s, dim e) sits at
- *   K: (((e/32)*2 + (s/4)%2)*4 + (e%32)/8)*64 + ((s/8)*4 + s%4)*8 + e%8
- *   V: ((e/16)*2 + s/8)*128 + (e%16)*8 + s%8
- * Token t of request i lives in block page_table[i][t / 16], slot t % 16. */
+/* KV pool of one layer: [n_blocks][n_kv][16][hd], a page holding 16 slots of hd values
+ * each, slot-major.  Token t of request i lives in block page_table[i][t / 16], slot t % 16. */
 static double kv_get(int bf16, const void *pool, int64_t idx) {
   return bf16 ? bf16_to_double(((const uint16_t *)pool)[idx]) : (double)((const float *)pool)[idx];
 }
@@ -388,25 +402,17 @@ static void kv_put(int bf16, void *pool, int64_t idx, double v) {
     ((float *)pool)[idx] = (float)v;
 }
 
-static int64_t page_base(int n_kv, int hd, int block, int kvh) {
-  return ((int64_t)block * n_kv + kvh) * (int64_t)(ORC_PAGE * hd);
-}
-
-static int64_t k_index(int n_kv, int hd, int block, int kvh, int slot, int dim) {
-  return page_base(n_kv, hd, block, kvh) + (((dim / 32) * 2 + (slot / 4) % 2) * 4 + (dim % 32) / 8) * 64 +
-         ((slot / 8) * 4 + slot % 4) * 8 + dim % 8;
-}
-
-static int64_t v_index(int n_kv, int hd, int block, int kvh, int slot, int dim) {
-  return page_base(n_kv, hd, block, kvh) + ((dim / 16) * 2 + slot / 8) * 128 + (dim % 16) * 8 + slot % 8;
+static int64_t kv_index(int n_kv, int hd, int block, int kvh, int slot, int dim) {
+  return (((int64_t)block * n_kv + kvh) * ORC_PAGE + slot) * hd + dim;
 }
 
 /* Causal attention of the new rows over each request's paged KV (one layer).
  * q: [M][n_q][hd]; out: [M][n_q][hd].  Row j of request i sits at position
- * ctx_len[i] + j and sees keys 0 .. ctx_len[i] + j. */
-int orc_paged_attention(int n_q, int n_kv, int hd, int bf16, const void *k_pool, const void *v_pool,
-                        const int32_t *page_table, int pt_stride, int B, const int32_t *ctx_len,
-                        const int32_t *n_new, const double *q, double *out) {
+ * ctx_len[i] + j and sees keys 0 .. ctx_len[i] + j.  acc32: the dot products, the
+ * softmax denominator and the weighted sum of values accumulate in fp32. */
+int orc_paged_attention(int n_q, int n_kv, int hd, int bf16, int acc32, const void *k_pool,
+                        const void *v_pool, const int32_t *page_table, int pt_stride, int B,
+                        const int32_t *ctx_len, const int32_t *n_new, const double *q, double *out) {
   int G = n_q / n_kv;
   int64_t *off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(B + 1));
   off[0] = 0;
@@ -427,23 +433,34 @@ int orc_paged_attention(int n_q, int n_kv, int hd, int bf16, const void *k_pool,
     for (int t = 0; t <= pos; t++) {
       int blk = page_table[(int64_t)i * pt_stride + t / ORC_PAGE];
       double dot = 0.0;
-      for (int e = 0; e < hd; e++)
-        dot += qv[e] * kv_get(bf16, k_pool, k_index(n_kv, hd, blk, kvh, t % ORC_PAGE, e));
-      s[t] = dot * scale;
+      float dot32 = 0.0f;
+      for (int e = 0; e < hd; e++) {
+        const double kk = kv_get(bf16, k_pool, kv_index(n_kv, hd, blk, kvh, t % ORC_PAGE, e));
+        if (acc32)
+          dot32 += (float)qv[e] * (float)kk;
+        else
+          dot += qv[e] * kk;
+      }
+      s[t] = (acc32 ? (double)dot32 : dot) * scale;
       if (s[t] > mx) mx = s[t];
     }
     double den = 0.0;
+    float den32 = 0.0f;
     for (int t = 0; t <= pos; t++) {
       s[t] = exp(s[t] - mx);
       den += s[t];
+      den32 += (float)s[t];
     }
+    if (acc32) den = den32;
     double *o = out + (r * n_q + hq) * hd;
     for (int e = 0; e < hd; e++) o[e] = 0.0;
     for (int t = 0; t <= pos; t++) {
       int blk = page_table[(int64_t)i * pt_stride + t / ORC_PAGE];
       double w = s[t] / den;
-      for (int e = 0; e < hd; e++)
-        o[e] += w * kv_get(bf16, v_pool, v_index(n_kv, hd, blk, kvh, t % ORC_PAGE, e));
+      for (int e = 0; e < hd; e++) {
+        const double vv = kv_get(bf16, v_pool, kv_index(n_kv, hd, blk, kvh, t % ORC_PAGE, e));
+        o[e] = acc32 ? (double)((float)o[e] + (float)w * (float)vv) : o[e] + w * vv;
+      }
     }
     free(s);
   }
@@ -502,15 +519,15 @@ int orc_forward(const orc_model *m, void *k_pool, void *v_pool, int n_blocks, in
       int slot = pos[r] % ORC_PAGE;
       for (int hh = 0; hh < nkv; hh++)
         for (int e = 0; e < hd; e++) {
-          kv_put(m->bf16, kl, k_index(nkv, hd, blk, hh, slot, e), kb[r * kd + hh * hd + e]);
-          kv_put(m->bf16, vl, v_index(nkv, hd, blk, hh, slot, e), vb[r * kd + hh * hd + e]);
+          kv_put(m->bf16, kl, kv_index(nkv, hd, blk, hh, slot, e), kb[r * kd + hh * hd + e]);
+          kv_put(m->bf16, vl, kv_index(nkv, hd, blk, hh, slot, e), vb[r * kd + hh * hd + e]);
         }
     }
-    orc_paged_attention(nq, nkv, hd, m->bf16, kl, vl, page_table, pt_stride, B, ctx_len, n_new,
-                        qb, ob);
+    orc_paged_attention(nq, nkv, hd, m->bf16, m->acc32, kl, vl, page_table, pt_stride, B, ctx_len,
+                        n_new, qb, ob);
     for (int64_t e = 0; e < M * qd; e++) ob[e] = act_round(m, ob[e]);
     linear(m, m->wo[l], ob, tmp, (int)M, qd, d);
-    for (int64_t e = 0; e < M * d; e++) h[e] += tmp[e];
+    residual_add(m, h, tmp, M * d);
 
     rmsnorm(m, m->mlp_norm[l], h, x, (int)M);
     linear(m, m->w_gate[l], x, gb, (int)M, d, F);
@@ -520,7 +537,7 @@ int orc_forward(const orc_model *m, void *k_pool, void *v_pool, int n_blocks, in
       gb[e] = act_round(m, g / (1.0 + exp(-g)) * ub[e]);   /* SwiGLU: silu(gate) * up */
     }
     linear(m, m->w_down[l], gb, tmp, (int)M, F, d);
-    for (int64_t e = 0; e < M * d; e++) h[e] += tmp[e];
+    residual_add(m, h, tmp, M * d);
   }
   rmsnorm(m, m->final_norm, h, x, (int)M);
   {
@@ -552,6 +569,16 @@ int orc_row_probs(const float *l, int V, float T, float *p) {
   float m, S;
   row_softmax_stats(l, V, T, &m, &S);
   for (int k = 0; k < V; k++) p[k] = prob_at(l, T, m, S, k);
+  return 0;
+}
+
+/* One projection y = x W^T as the forward computes it (fp64, or fp32 sums with acc32);
+ * W holds fp32 values, x rows of `in` values. */
+int orc_linear_apply(const float *W, const double *x, double *y, int rows, int in, int outn, int acc32) {
+  orc_model m;
+  memset(&m, 0, sizeof(m));
+  m.acc32 = acc32;
+  linear(&m, W, x, y, rows, in, outn);
   return 0;
 }
 

@@ -42,7 +42,8 @@ EXPORTS = ("wisp_workspace_size", "wisp_logits_workspace_size", "wisp_accept_wor
            "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
            "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule", "wisp_kvm_create",
            "wisp_kvm_destroy", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit", "wisp_kvm_release",
-           "wisp_kvm_get_stats", "wisp_draft_stats_workspace_size", "wisp_draft_stats", "wisp_reject_predict")
+           "wisp_kvm_get_stats", "wisp_draft_stats_workspace_size", "wisp_draft_stats", "wisp_reject_predict",
+           "wisp_gemm_plan")
 
 
 class WispError(RuntimeError):
@@ -130,6 +131,7 @@ def _load():
                                  _VP, _VP, _VP, C.c_size_t, _VP]
     L.wisp_uniform.argtypes = [C.c_uint64, C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint32, _VP, _VP]
     L.wisp_check.argtypes = [_VP, _VP]
+    L.wisp_gemm_plan.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32)]
     L.wisp_profile_enable.argtypes = [C.c_int]
     L.wisp_profile_read.argtypes = [C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64),
                                     C.POINTER(C.c_double), C.POINTER(C.c_double)]
@@ -153,7 +155,7 @@ def _load():
     L.wisp_draft_stats.argtypes = [_VP, C.c_int32, C.c_int32, C.c_int64, C.c_float, _VP, _VP, C.c_size_t, _VP]
     L.wisp_reject_predict.argtypes = [C.POINTER(wisp_reject_mlp), _VP, C.c_int32, _VP, _VP]
     for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
-                 "wisp_check", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
+                 "wisp_check", "wisp_gemm_plan", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
                  "wisp_schedule", "wisp_kvm_create", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit",
                  "wisp_kvm_release", "wisp_kvm_get_stats", "wisp_draft_stats", "wisp_reject_predict"):
         getattr(L, name).restype = C.c_int
@@ -542,11 +544,22 @@ class KVManager:
             pass
 
 
+def gemm_plan(M: int, N: int, K: int) -> dict:
+    """The launch plan of one bf16 projection (wisp_gemm_plan): kernel variant, row blocks,
+    32-row fragments per block, K ranges."""
+    out = (C.c_int32 * 4)()
+    _ok(lib.wisp_gemm_plan(int(M), int(N), int(K), out))
+    return dict(kind=out[0], rb=out[1], mt=out[2], splits=out[3])
+
+
 def wisp_check(workspace, stream=None):
     _ok(lib.wisp_check(_dev(workspace, "workspace"), _stream(stream)))
 
 
 def workspace(nbytes: int, device="cuda"):
-    """A device byte buffer for the workspace argument (torch allocation)."""
+    """A device byte buffer for the workspace argument (torch allocation), its fault record
+    (the first 256 bytes) cleared as the library requires before first use."""
     import torch
-    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    ws[:256].zero_()
+    return ws

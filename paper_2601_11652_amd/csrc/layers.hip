@@ -203,8 +203,10 @@ void gather_ints(const int32_t *src, const int32_t *idx, int n, int32_t *dst, hi
 // qkv partials -> RoPE (rotate-half) -> q buffer, k/v appended into the pages in place
 // ---------------------------------------------------------------------------------------
 // Grid (row, group of 8 heads); each thread owns 8 consecutive dims of one head.  The
-// rotate-half partner (dims i and i + hd/2) sits hd/16 lanes away and is exchanged with a
-// shuffle; q and K are written as 16-byte stores (8 consecutive dims are contiguous in
+// rotate-half partner (dims i and i + hd/2) belongs to the thread hd/16 places further
+// round the same head; partners are exchanged through LDS, which pairs the right threads
+// for every head_dim (a head need not sit inside one wave, nor at a power-of-two lane
+// offset).  q and K are written as 16-byte stores (8 consecutive dims are contiguous in
 // the K page layout), V element by element.
 constexpr int kRopeHeadsPerBlock = 8;
 
@@ -234,7 +236,8 @@ __global__ __launch_bounds__(256) void qkv_rope_append_kernel(StepDesc d, const 
   const int i0 = (threadIdx.x % tph) * 8;          // first dim of this thread
   const int h2 = hd / 2;
   const int N = nh * hd;
-  float v[8];
+  __shared__ float xch[kRopeHeadsPerBlock * 256];   // 8 values per thread, hd <= 256
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (head < nh) {
     const float *p = part + (int64_t)r * N + head * hd + i0;
     const int64_t stride = (int64_t)M * N;
@@ -243,10 +246,14 @@ __global__ __launch_bounds__(256) void qkv_rope_append_kernel(StepDesc d, const 
     v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w;
     v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
   }
-  // rotate-half partner values (whole waves take part in the shuffle)
+  // rotate-half partner values: thread t of a head pairs with thread (t + tph/2) mod tph
+#pragma unroll
+  for (int e = 0; e < 8; ++e) xch[threadIdx.x * 8 + e] = v[e];
+  __syncthreads();
+  const int partner = (threadIdx.x / tph) * tph + (threadIdx.x % tph + tph / 2) % tph;
   float w[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) w[e] = __shfl_xor(v[e], hd / 16);
+  for (int e = 0; e < 8; ++e) w[e] = xch[partner * 8 + e];
   if (head >= nh) return;
   const int req = d.row_req[r], pos = d.row_pos[r];
   if (head < nq + nkv) {   // RoPE on q and k heads

@@ -3,12 +3,14 @@
 // token -- drawn from norm(max(0, p_R - q_R)) after a rejection (the residual that makes
 // speculative sampling lossless) and from p after a fully accepted block.
 //
-// Two kernels per batch: per-row softmax statistics (max and sum of exponentials of
-// z = logits / T, a vocabulary-wide two-pass reduction), then one workgroup per request
-// runs the sequential accept scan and the vocabulary-wide exponential race that samples
-// the extra token (argmax of score - ln(-ln u), no prefix sums, so the result does not
-// depend on reduction order).  All random draws come from Philox4x32-10 keyed by the
-// seed and counted by (index, row, request, purpose).
+// Four launches per batch, each over vocabulary chunks of 8192 entries: the row maxima of
+// z = logits / T (argmax at T = 0), the fp64 sums of exp(z - max), then one workgroup per
+// (request, chunk) decides every draft in parallel (thread j - 1 takes draft j; R is the
+// smallest rejected j, an integer minimum) and runs its chunk of the exponential race that
+// samples the extra token (argmax of score - ln(-ln u): no prefix sums, so the result does
+// not depend on reduction order), and a last kernel combines the chunks' winners in fixed
+// order.  All random draws come from Philox4x32-10 keyed by the seed and counted by
+// (index, row, request, purpose).
 #pragma clang fp contract(off)
 #include "common.h"
 #include "kernels.h"

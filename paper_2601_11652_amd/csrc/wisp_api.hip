@@ -656,7 +656,6 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
     if (!target_logits) target_logits = reinterpret_cast<float *>(ws + p.total);
     if ((st = upload(p, ws, s)) != WISP_OK) return st;
     StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
-    clear_ints(sd.err, 1, s);
     if (p.bf16)
       st = run_forward<uint16_t>(p, model, kv, sd, ws, tokens, target_logits, s);
     else
@@ -701,7 +700,6 @@ wisp_status wisp_accept(const wisp_batch_desc *desc, int32_t vocab, const float 
     char *ws = (char *)workspace;
     if ((st = upload(p, ws, s)) != WISP_OK) return st;
     StepDesc sd = step_desc(p, ws, desc, 0);
-    clear_ints(sd.err, 1, s);
     sampler(sd, p.B, p.M, vocab, logits, tokens, draft_probs, desc->temperature, rng_seed,
             sampler_scratch(p, ws), accept_len, out_tokens, s);
     return hip_check("sampler launch");
@@ -728,7 +726,6 @@ wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wis
     char *ws = (char *)workspace;
     if ((st = upload(p, ws, s)) != WISP_OK) return st;
     StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
-    clear_ints(sd.err, 1, s);
     if (p.bf16) {
       const AttnItem *items = reinterpret_cast<const AttnItem *>(ws + p.w_desc + p.i_items * 4);
       const AttnGroup *groups = reinterpret_cast<const AttnGroup *>(ws + p.w_desc + p.i_groups * 4);
@@ -782,6 +779,20 @@ wisp_status wisp_profile_reset(void) {
       g_prof.ms[k] = g_prof.bytes[k] = g_prof.flops[k] = 0.0;
       g_prof.launches[k] = 0;
     }
+    return WISP_OK;
+  });
+}
+
+wisp_status wisp_gemm_plan(int32_t M, int32_t N, int32_t K, int32_t out[4]) {
+  return guarded("wisp_gemm_plan", [&]() -> wisp_status {
+    if (!out) return fail(WISP_E_INVALID, "out is NULL");
+    if (M < 1 || N < 1 || K < 1 || N % 32 || K % 16)
+      return fail(WISP_E_INVALID, "M, N, K must be positive, N a multiple of 32, K of 16");
+    const GemmCfg c = gemm_bf16_plan(M, N, K);
+    out[0] = c.kind;
+    out[1] = c.rb;
+    out[2] = c.mt;
+    out[3] = c.splits;
     return WISP_OK;
   });
 }

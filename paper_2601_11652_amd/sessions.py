@@ -31,7 +31,7 @@ import time
 
 import numpy as np
 
-from . import (PAGE, BatchDesc, KVManager, KVPool, wisp_draft_stats, wisp_reject_predict, wisp_verify,
+from . import (PAGE, BatchDesc, KVManager, KVPool, wisp_verify,
                wisp_workspace_size, workspace)
 from .records import command_line
 
@@ -53,9 +53,6 @@ class Sessions:
         self.seed = seed
         self.t_draft, self.sigma = t_draft, sigma
         self.max_rows = max_rows
-        self.sigma_range = None     # (lo, hi): per drafted token, sigma ~ U[lo, hi]
-        self.controller = None      # (RejectMLP, threshold): stop at the first predicted rejection
-        self.trace = None           # a list to log every drafted token's features in
         self.seq = {}
         self.gen = torch.Generator(device="cuda")
         self.gen.manual_seed(seed)
@@ -107,14 +104,7 @@ class Sessions:
 
     def draft(self, sids, gammas, rnd: int):
         """Draft up to gamma_i tokens per session with the device-side model.  Returns the
-        drafts (list of lists) and the q rows (fp32 [sum gamma][V], request-major).
-
-        With a controller (Sec. 4.1's stop-at-first-predicted-rejection), the statistics of
-        each drafted token's distribution (wisp_draft_stats on the draft logits) and its
-        position feed the rejection predictor (wisp_reject_predict); a session stops
-        drafting after the first token whose predicted acceptance falls below the
-        controller's threshold (that token is still sent).  With `self.trace` set, every
-        drafted token's features are appended to it as (session, position, features)."""
+        drafts (list of lists) and the q rows (fp32 [sum gamma][V], request-major)."""
         torch = self.torch
         B = len(sids)
         n = np.array([len(self.seq[s]) for s in sids], np.int64)
@@ -123,14 +113,12 @@ class Sessions:
         drafts = [[] for _ in range(B)]
         qrows = [[] for _ in range(B)]
         req = np.asarray(sids, np.int64).astype(np.uint32)
-        stopped = np.zeros(B, bool)
-        want_stats = self.controller is not None or self.trace is not None
         for grp in self._chunks(n - cached):
             gs = [sids[i] for i in grp]
             table, ev = self.dm.reserve(gs, (n[grp] + g[grp] - 1).astype(np.int32), self.stride)
             assert ev == 0, "the draft-side pool holds every session"
             for j in range(int(g[grp].max())):
-                act = [k for k, i in enumerate(grp) if g[i] > j and not stopped[i]]
+                act = [k for k, i in enumerate(grp) if g[i] > j]
                 if not act:
                     break
                 idx = [grp[k] for k in act]
@@ -146,33 +134,12 @@ class Sessions:
                                              pre.astype(np.int32), table[act], toks, None,
                                              (self.seed << 20) + 2 * rnd + 1, req[idx])
                 eps = torch.randn(logits.shape, generator=self.gen, device="cuda")
-                if self.sigma_range is None:
-                    z = logits / self.t_draft + self.sigma * eps
-                else:                      # a per-token error scale: drafts of varying difficulty
-                    lo, hi = self.sigma_range
-                    sg = lo + (hi - lo) * torch.rand(logits.shape[0], 1, generator=self.gen, device="cuda")
-                    z = logits / self.t_draft + sg * eps
+                z = logits / self.t_draft + self.sigma * eps
                 q = torch.softmax(z, dim=-1)
                 y = torch.multinomial(q, 1, generator=self.gen)[:, 0].tolist()
                 for r, i in enumerate(idx):
                     drafts[i].append(int(y[r]))
                     qrows[i].append(q[r])
-                if want_stats:
-                    z = z.contiguous()
-                    st = torch.empty(len(idx), 4, dtype=torch.float32, device="cuda")
-                    wisp_draft_stats(z, self.shape.vocab, 1.0, st)
-                    feats = torch.cat([st, torch.full((len(idx), 1), float(j), device="cuda")], dim=1).contiguous()
-                    if self.trace is not None:
-                        fh = feats.cpu().numpy()
-                        for r, i in enumerate(idx):
-                            self.trace.append((sids[i], j, fh[r]))
-                    if self.controller is not None:
-                        mlp, threshold = self.controller
-                        pa = torch.empty(len(idx), dtype=torch.float32, device="cuda")
-                        wisp_reject_predict(mlp, feats, pa)
-                        for r, p_accept in enumerate(pa.tolist()):
-                            if p_accept < threshold:
-                                stopped[idx[r]] = True
         return drafts, qrows
 
     def verify(self, sids, drafts, qrows, rnd: int):

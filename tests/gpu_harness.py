@@ -30,6 +30,68 @@ def to_host_storage(t: torch.Tensor) -> np.ndarray:
     return t.numpy()
 
 
+def pools_to_dev(pools, hd: int):
+    """Oracle pools (slot-major pages, [..., 16 * hd]) -> device pools in the library's page
+    layout (the K and V page orders of the C ABI)."""
+    k = wi.pages_from_slots(pools[0].reshape(pools[0].shape[:-1] + (wi.PAGE, hd)), "k")
+    v = wi.pages_from_slots(pools[1].reshape(pools[1].shape[:-1] + (wi.PAGE, hd)), "v")
+    return to_dev(k), to_dev(v)
+
+
+def pools_from_dev(k: torch.Tensor, v: torch.Tensor, hd: int):
+    """Device pools in the library's page layout -> host storage, slot-major pages."""
+    out = []
+    for t, which in ((k, "k"), (v, "v")):
+        p = wi.slots_from_pages(to_host_storage(t), which, hd)
+        out.append(np.ascontiguousarray(p.reshape(p.shape[:-2] + (wi.PAGE * hd,))))
+    return out[0], out[1]
+
+
+def written_mask(pool_shape, page_table, ctx_len, n_new, hd: int) -> np.ndarray:
+    """Boolean mask over a slot-major pool [layers][blocks][n_kv][16 * hd]: the slots at
+    positions ctx_len[i] .. ctx_len[i] + n_new[i] - 1 of every request."""
+    m = np.zeros(pool_shape, bool)
+    v = m.reshape(pool_shape[:3] + (wi.PAGE, hd))
+    for i in range(len(ctx_len)):
+        for pos in range(int(ctx_len[i]), int(ctx_len[i]) + int(n_new[i])):
+            v[:, page_table[i, pos // wi.PAGE], :, pos % wi.PAGE, :] = True
+    return m
+
+
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    """One unit in the last place of bf16 at |x| (8 significant bits; the smallest normal's
+    quantum below it)."""
+    a = np.maximum(np.abs(np.asarray(x, np.float64)), 2.0 ** -126)
+    return 2.0 ** (np.floor(np.log2(a)) - 7)
+
+
+def check_written(pools_gpu, pools_ref, pools_before, page_table, ctx_len, n_new, hd: int, bf16: bool,
+                  f32_atol: float = 1e-4, floor=None):
+    """K/V written at the new positions match the oracle's, every other slot is untouched
+    bit for bit.  bf16: within one bf16 ulp of the oracle's value (two correct fp32
+    accumulation orders may round a value on either side of a bf16 boundary), or, where
+    `floor` gives a per-layer pair (K, V) of the oracle's own floor, within twice it.  fp32:
+    within f32_atol."""
+    worst = 0.0
+    for w in range(2):
+        g = storage_to_f64(pools_gpu[w])
+        r = storage_to_f64(pools_ref[w])
+        before = storage_to_f64(pools_before[w])
+        written = written_mask(g.shape, page_table, ctx_len, n_new, hd)
+        for l in range(g.shape[0]):
+            gl, rl = g[l][written[l]], r[l][written[l]]
+            if gl.size == 0:
+                continue
+            bound = bf16_ulp(rl) if bf16 else np.full(rl.shape, f32_atol)
+            if floor is not None:
+                bound = np.maximum(bound, 2.0 * floor[l][w])
+            ratio = float((np.abs(gl - rl) / bound).max())
+            assert ratio <= 1.0, ("KV"[w], l, ratio, float(np.abs(gl - rl).max()))
+            worst = max(worst, ratio)
+        np.testing.assert_array_equal(g[~written], before[~written])
+    return worst
+
+
 def gpu_model(shape: wi.ModelShape, seed: int = wi.MASTER_SEED) -> W.GpuModel:
     glob = wi.global_weights(shape, seed, "cuda")
     return W.GpuModel(shape, lambda l: wi.layer_weights(shape, l, seed, "cuda"), glob)
@@ -70,9 +132,10 @@ class Workload:
 
 
 def run_gpu(gm: W.GpuModel, wl: Workload):
-    """One wisp_verify call on the workload; returns numpy outputs and the pools after it."""
+    """One wisp_verify call on the workload; returns numpy outputs and the pools after it
+    (slot-major, as the oracle holds them)."""
     mix = wl.mix
-    kv = W.KVPool(to_dev(wl.pools0[0]), to_dev(wl.pools0[1]))
+    kv = W.KVPool(*pools_to_dev(wl.pools0, mix.shape.head_dim))
     pt = to_dev(wl.pt)
     desc = W.BatchDesc(mix.ctx_len, mix.gamma, pt, wl.T, mix.req_id)
     ws = W.workspace(W.wisp_workspace_size(gm.c, desc))
@@ -85,7 +148,7 @@ def run_gpu(gm: W.GpuModel, wl: Workload):
     W.wisp_check(ws)
     torch.cuda.synchronize()
     return (acc.cpu().numpy(), out.cpu().numpy(), logits.cpu().numpy(),
-            (to_host_storage(kv.k), to_host_storage(kv.v)))
+            pools_from_dev(kv.k, kv.v, mix.shape.head_dim))
 
 
 def rel_row_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
@@ -139,3 +202,18 @@ def compare_decisions(acc_gpu, out_gpu, ref: oracle.AcceptResult, gamma, tokens,
         np.testing.assert_array_equal(o[:L], tokens[off[i] + 1:off[i] + 1 + L])
         assert o[L] >= 0 and np.all(o[L + 1:] == -1)
     return n_dec, mism, unflagged
+
+
+def check_decisions_on_gpu_logits(acc_gpu, out_gpu, logits_gpu, tokens, q, gamma, temperature, seed,
+                                  req_id=None):
+    """The acceptance contract on identical logits: the oracle's acceptance run on the GPU's
+    own logits must take the GPU's decisions.  A mismatch is allowed only on a flagged
+    near-tie (|u - p/q| < 1e-3, or top-two race keys within 1e-5 relative) and such
+    mismatches stay under 0.1 % of the decisions (at most one below 1000 decisions).
+    Returns (decisions, mismatches)."""
+    ref = oracle.accept(logits_gpu, tokens, q, gamma, temperature, seed, req_id=req_id)
+    n_dec, mism, unflagged = compare_decisions(acc_gpu, out_gpu, ref, np.asarray(gamma), tokens, 1e-3, 1e-5)
+    assert not unflagged, ("unflagged decision mismatches on identical logits", unflagged)
+    assert mism <= max(1, int(1e-3 * n_dec)), (mism, n_dec)
+    return n_dec, mism
+

@@ -187,3 +187,19 @@ def test_binding_rejects_host_and_mistyped_tensors(W):
                       torch.zeros(256, dtype=torch.uint8))
     with pytest.raises(ValueError, match="unit column stride"):
         W.wisp_draft_stats(torch.zeros((8, 4)).t(), 8, 1.0, torch.zeros((4, 4)))
+
+
+def test_gemm_plan_of_the_wide_projections(W):
+    """The plan picks the 64-column weight ring (variant 2) for outputs of >= 16384
+    columns: gate/up and the LM head of the wide test model (d_model 512, d_ff 8192,
+    vocabulary 32768) in one and in two row blocks, with two K ranges for gate/up; the
+    32-column ring below that width."""
+    for M, rb in ((44, 1), (510, 2)):
+        gu = W.gemm_plan(M, 2 * 8192, 512)
+        lm = W.gemm_plan(M, 32768, 512)
+        assert gu["kind"] == 2 and lm["kind"] == 2, (gu, lm)
+        assert gu["rb"] == rb and lm["rb"] == rb, (gu, lm)
+        assert gu["splits"] == 2, gu
+    assert W.gemm_plan(44, 1024, 256)["kind"] == 1
+    with pytest.raises(W.WispError):
+        W.gemm_plan(0, 1024, 256)

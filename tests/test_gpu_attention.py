@@ -40,8 +40,10 @@ def _case(ctx, gamma, n_q, n_kv, hd, bf16, seed):
         kp, vp, qs = [r(a).astype(np.uint16) for a in (kd, vd, q)]
     else:
         kp, vp, qs = kd, vd, q
+    # the oracle reads slot-major pages, the library its own page order
+    kn, vn = kp.reshape(n_blocks, n_kv, 16 * hd), vp.reshape(n_blocks, n_kv, 16 * hd)
     kp, vp = wi.pages_from_slots(kp, "k"), wi.pages_from_slots(vp, "v")
-    return ctx, gamma, pt, kp, vp, qs
+    return ctx, gamma, pt, kp, vp, qs, kn, vn
 
 
 def _f64(a):
@@ -58,7 +60,7 @@ def _f64(a):
 @pytest.mark.parametrize("bf16", [True, False])
 def test_attention_matches_oracle(ctx, gamma, n_q, n_kv, hd, bf16):
     log(f"attention ctx={ctx} gamma={gamma} nq={n_q} nkv={n_kv} hd={hd} bf16={bf16}")
-    ctx, gamma, pt, kp, vp, q = _case(ctx, gamma, n_q, n_kv, hd, bf16, seed=sum(ctx) + n_q)
+    ctx, gamma, pt, kp, vp, q, kn, vn = _case(ctx, gamma, n_q, n_kv, hd, bf16, seed=sum(ctx) + n_q)
     shape = wi.ModelShape("attn", 1, 256, n_q, n_kv, hd, 256, 256, "bf16" if bf16 else "f32", 1e4)
     model = W.GpuModel.shape_only(shape)
     kv = W.KVPool(to_dev(kp[None]), to_dev(vp[None]))
@@ -70,7 +72,7 @@ def test_attention_matches_oracle(ctx, gamma, n_q, n_kv, hd, bf16):
     W.wisp_attention(model, kv, desc, dq, out, ws)
     W.wisp_check(ws)
     got = _f64(out.cpu().view(torch.int16).numpy().view(np.uint16)) if bf16 else out.cpu().numpy().astype(np.float64)
-    want = oracle.paged_attention(_f64(q), kp, vp, pt, ctx, gamma + 1, n_kv, bf16)
+    want = oracle.paged_attention(_f64(q), kn, vn, pt, ctx, gamma + 1, n_kv, bf16)
     err = np.abs(got - want)
     if bf16:
         assert err.max() < 2.5e-2, err.max()
@@ -84,7 +86,7 @@ def test_fp32_attention_at_its_longest_context():
     documented maximum of 32768 tokens per request that is 128 KB in one workgroup."""
     ctx, gamma = [32768 - 5], [4]
     log(f"fp32 attention at {ctx[0] + gamma[0] + 1} tokens")
-    ctx, gamma, pt, kp, vp, q = _case(ctx, gamma, 4, 2, 32, False, seed=32768)
+    ctx, gamma, pt, kp, vp, q, kn, vn = _case(ctx, gamma, 4, 2, 32, False, seed=32768)
     shape = wi.ModelShape("attn", 1, 128, 4, 2, 32, 128, 256, "f32", 1e4)
     model = W.GpuModel.shape_only(shape)
     kv = W.KVPool(to_dev(kp[None]), to_dev(vp[None]))
@@ -94,7 +96,7 @@ def test_fp32_attention_at_its_longest_context():
     out = torch.zeros_like(dq)
     W.wisp_attention(model, kv, desc, dq, out, ws)
     W.wisp_check(ws)
-    want = oracle.paged_attention(q.astype(np.float64), kp, vp, pt, ctx, gamma + 1, 2, False)
+    want = oracle.paged_attention(q.astype(np.float64), kn, vn, pt, ctx, gamma + 1, 2, False)
     got = out.cpu().numpy().astype(np.float64)
     # each output sums 32768 fp32 products in order: relative bar of the fp32 path
     rel = np.abs(got - want).max() / np.abs(want).max()

@@ -3,28 +3,29 @@ benchmark times: the whole batch goes through ONE wisp_verify call (same batch
 descriptor, page table and workspace sizing), and the oracle recomputes sampled
 requests one at a time on the host.
 
-Tolerance at depth.  The bf16 rounding contract has a noise floor of its own: moving
-two entries of one embedding row by one bf16 ulp moves the oracle's own 8B logits by
-about 0.04 max-abs after one layer and 0.18 after 32, because every later rounding
-point turns a sub-ulp change into whole-ulp flips.  Any implementation that accumulates
-in a different order than the oracle's fp64 sums lands on that floor (measured: GPU vs
-oracle 0.8-1.1x the floor at depths 1 to 32 of the 8B model).  So each quantity Q
-(logits, the K and V rows written at each layer) is checked against
-max(bound_Q, 2 * floor_Q), where floor_Q is the oracle's own change of Q under that
-1-ulp perturbation, computed in the test; bound_Q is 2e-2 for logits and one bf16 ulp
-at |x| < 16 for KV.  A wrong index, position, page or row shows up as an error far above
-the floor.
+Tolerance at depth.  The bf16 rounding contract has a noise floor of its own: two correct
+implementations that sum in different orders round some values on different sides of a
+bf16 boundary, and every later rounding point carries those one-ulp flips on.  The floor
+is measured, not assumed: the oracle runs each sampled request twice, with fp64 sums (the
+reference) and with fp32 sums in natural index order (another correct order), and
+floor_Q = max |Q_fp32 - Q_fp64| for each checked quantity Q (logits; the K and V rows
+written at each layer).  The GPU must then stay within
 
-Per sampled request (drafts from the oracle's own autoregressive fixture, so the
-acceptance chain is exercised): logits and written K/V rows as above, every other slot
-of its pages unchanged bit for bit, decisions equal to the oracle's except where the
-observed logit gap could flip them (acceptance margin widened by exp(2 gap) - 1, race
-margin by 4 gap, residual resample exempt).  For every request of the batch (drafts from
-the model-independent seeded fixture): finite logits, an accepted prefix equal to the
-drafts, one valid extra token, -1 padding, and no error flag.
+  logits: max-abs  <= max(2e-2, 2 * floor), mean-abs <= max(2e-3, 2 * mean floor);
+  K / V:  per value <= max(one bf16 ulp of the oracle's value, 2 * the layer's floor).
 
-Sampled requests: the first, the longest context, the largest gamma, and a plain-decode
-(gamma = 0) request where the mix has one.
+A wrong index, position, page, row or a dropped term shows up far above the floor.
+
+Decisions.  Bit-exact on identical logits: the oracle's acceptance run on the GPU's logits
+of the WHOLE batch must take the GPU's decisions, except on flagged near-ties (< 0.1 %).
+End to end (each side on its own logits), the sampled requests' decisions must agree where
+the observed logit gap cannot flip them (acceptance margin widened by exp(2 gap) - 1, race
+margin by 4 gap, residual resample exempt).  Every request: finite logits, an accepted
+prefix equal to the drafts, one valid extra token, -1 padding, no error flag.
+
+Sampled requests (drafts from the oracle's own autoregressive fixture): the first, a
+plain-decode request where the mix has one, the longest context and the largest gamma;
+the other requests take model-independent seeded drafts.
 """
 import numpy as np
 import pytest
@@ -34,12 +35,14 @@ import oracle
 import paper_2601_11652_amd as W
 import wisp_inputs as wi
 from oracle import fixtures as fx
-from gpu_harness import compare_decisions, gpu_model, log, storage_to_f64, to_host_storage
+from gpu_harness import (bf16_ulp, check_decisions_on_gpu_logits, compare_decisions, gpu_model, log,
+                         storage_to_f64, to_host_storage)
 
 pytestmark = pytest.mark.gpu
 
-LOGIT_ATOL = 2e-2      # bf16 logits bound
-KV_ATOL = 6e-2         # one bf16 ulp at |x| < 16
+LOGIT_ATOL = 2e-2      # bf16 logits bound, max-abs
+LOGIT_MEAN = 2e-3      # bf16 logits bound, mean-abs
+FLOOR_FACTOR = 2.0     # allowance over the measured fp32-vs-fp64 floor
 
 
 def _samples(mix, n):
@@ -56,8 +59,8 @@ def _samples(mix, n):
 
 def _oracle_request(model, mix, i, roots):
     """Request i reproduced alone on the host: its context pages, oracle drafts, the
-    oracle's logits of its gamma + 1 rows and its pools after the step, and the same two
-    outputs with the root token's embedding row moved by one ulp in two entries."""
+    oracle's logits of its gamma + 1 rows and its pools after the step, with fp64 sums and
+    again with fp32 sums (the floor)."""
     s = mix.shape
     sub = wi.custom_mix(s, [mix.ctx_len[i]], [mix.gamma[i]], seed=mix.seed, name=mix.config)
     sub.t_draft[:] = mix.t_draft[i]
@@ -71,11 +74,10 @@ def _oracle_request(model, mix, i, roots):
     del work
     after = (before[0].copy(), before[1].copy())
     logits = oracle.forward(model, after[0], after[1], pt, sub.ctx_len, sub.rows, toks[0])
-    pert = (before[0].copy(), before[1].copy())
-    with fx.perturbed_embedding(model, toks[0][0]):
-        logits_p = oracle.forward(model, pert[0], pert[1], pt, sub.ctx_len, sub.rows, toks[0])
+    after32 = (before[0].copy(), before[1].copy())
+    logits32 = oracle.forward(model, after32[0], after32[1], pt, sub.ctx_len, sub.rows, toks[0], acc32=True)
     return dict(tokens=toks[0], q=qs[0], logits=logits, before=before, after=after,
-                logits_p=logits_p, after_p=pert)
+                logits32=logits32, after32=after32)
 
 
 def _gather_pages(pool: torch.Tensor, blocks: np.ndarray) -> np.ndarray:
@@ -84,7 +86,7 @@ def _gather_pages(pool: torch.Tensor, blocks: np.ndarray) -> np.ndarray:
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("config,n_samples", [("8b_b32", 3), ("8b_b256", 2), ("8b_dyn128", 3), ("70b_b64", 1)])
+@pytest.mark.parametrize("config,n_samples", [("8b_b32", 4), ("8b_b256", 3), ("8b_dyn128", 4), ("70b_b64", 2)])
 def test_full_size_verify(config, n_samples):
     mix = wi.make_mix(config)
     s = mix.shape
@@ -142,35 +144,45 @@ def test_full_size_verify(config, n_samples):
         np.testing.assert_array_equal(o[:L], tokens_np[off[i] + 1:off[i] + 1 + L])
         assert 0 <= o[L] < s.vocab and np.all(o[L + 1:] == -1), (i, o)
 
-    # --- sampled requests against the oracle --------------------------------------------
+    # --- decisions on identical logits: the whole batch ---------------------------------
     seed = wi.verify_seed(mix)
-    kidx = wi.k_page_index(s.head_dim)
-    vidx = wi.v_page_index(s.head_dim)
+    logits_np = logits.cpu().numpy()
+    n_id, m_id = check_decisions_on_gpu_logits(acc_np, out_np, logits_np, tokens_np, q_np, mix.gamma, 1.0, seed,
+                                               req_id=mix.req_id)
+    log(f"  whole batch on the GPU's own logits: {n_id} decisions, {m_id} flagged mismatches")
+
+    # --- sampled requests against the oracle --------------------------------------------
     for i, r in ref.items():
         g = int(mix.gamma[i])
         lref = r["logits"]
-        lg = logits[off[i]:off[i + 1]].cpu().numpy()
-        err = np.abs(lg - lref).max()
-        floor = np.abs(r["logits_p"] - lref).max()
-        log(f"  request {i}: logits max-abs error {err:.3e}, oracle 1-ulp floor {floor:.3e} "
-            f"(|ref| max {np.abs(lref).max():.2f})")
-        assert err <= max(LOGIT_ATOL, 2.0 * floor), (i, err, floor)
+        lg = logits_np[off[i]:off[i + 1]]
+        d = np.abs(lg - lref)
+        fl = np.abs(r["logits32"] - lref)
+        log(f"  request {i}: logits max-abs error {d.max():.3e} (floor {fl.max():.3e}), mean-abs "
+            f"{d.mean():.3e} (floor {fl.mean():.3e}), |ref| max {np.abs(lref).max():.2f}")
+        assert d.max() <= max(LOGIT_ATOL, FLOOR_FACTOR * fl.max()), (i, d.max(), fl.max())
+        assert d.mean() <= max(LOGIT_MEAN, FLOOR_FACTOR * fl.mean()), (i, d.mean(), fl.mean())
 
         blocks = pt_np[i, :r["before"][0].shape[1]]
-        for w, (pool, idx) in enumerate(((kv.k, kidx), (kv.v, vidx))):
-            got = storage_to_f64(_gather_pages(pool, blocks))
+        hd = s.head_dim
+        for w, (pool, which) in enumerate(((kv.k, "k"), (kv.v, "v"))):
+            pages = wi.slots_from_pages(_gather_pages(pool, blocks), which, hd)     # [L][pages][kv][16][hd]
+            got = storage_to_f64(pages.reshape(pages.shape[:3] + (-1,)))
             exp = storage_to_f64(r["after"][w])
-            expp = storage_to_f64(r["after_p"][w])
+            exp32 = storage_to_f64(r["after32"][w])
             pre = storage_to_f64(r["before"][w])
             written = np.zeros(got.shape[1:], bool)
+            wv = written.reshape(written.shape[:2] + (wi.PAGE, hd))
             for pos in range(int(mix.ctx_len[i]), int(mix.ctx_len[i]) + g + 1):
-                written[pos // wi.PAGE, :, idx[pos % wi.PAGE]] = True
+                wv[pos // wi.PAGE, :, pos % wi.PAGE, :] = True
             worst = 0.0
             for l in range(s.n_layers):
-                e_l = np.abs(got[l][written] - exp[l][written]).max()
-                f_l = np.abs(expp[l][written] - exp[l][written]).max()
-                assert e_l <= max(KV_ATOL, 2.0 * f_l), (i, "KV"[w], l, e_l, f_l)
-                worst = max(worst, e_l / max(KV_ATOL, 2.0 * f_l))
+                e_l = np.abs(got[l][written] - exp[l][written])
+                f_l = np.abs(exp32[l][written] - exp[l][written]).max()
+                bound = np.maximum(bf16_ulp(exp[l][written]), FLOOR_FACTOR * f_l)
+                ratio = float((e_l / bound).max())
+                assert ratio <= 1.0, (i, "KV"[w], l, float(e_l.max()), f_l)
+                worst = max(worst, ratio)
             np.testing.assert_array_equal(got[:, ~written], pre[:, ~written])
             log(f"  request {i}: {'KV'[w]} rows written in place, worst error / bound {worst:.2f}")
 
@@ -178,8 +190,9 @@ def test_full_size_verify(config, n_samples):
                             req_id=mix.req_id[i:i + 1])
         n_dec, mism, unflagged = compare_decisions(acc_np[i:i + 1], out_np[off[i]:off[i + 1]], res,
                                                    mix.gamma[i:i + 1], r["tokens"], 1e-3, 1e-3,
-                                                   residual_exempt=True, logit_gap=err)
-        log(f"  request {i}: oracle L={int(res.accept_len[0])} gpu L={int(acc_np[i])}, mismatches {mism}")
+                                                   residual_exempt=True, logit_gap=float(d.max()))
+        log(f"  request {i}: oracle L={int(res.accept_len[0])} gpu L={int(acc_np[i])}, end-to-end "
+            f"mismatches {mism}")
         assert not unflagged, (i, unflagged)
     del gm, kv, logits, ws
     torch.cuda.empty_cache()

@@ -22,7 +22,7 @@ import oracle
 import paper_2601_11652_amd as W
 import wisp_inputs as wi
 from oracle import fixtures as fx
-from gpu_harness import gpu_model, log, to_dev
+from gpu_harness import gpu_model, log, pools_to_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +64,7 @@ def test_first_emitted_token_follows_the_target(T):
     gm = gpu_model(s)
     kp, vp = fx.empty_pools(s, 1 + B)
     kp[:, 0], vp[:, 0] = k0[:, 0], v0[:, 0]
-    kv = W.KVPool(to_dev(kp), to_dev(vp))
+    kv = W.KVPool(*pools_to_dev((kp, vp), s.head_dim))
     pt = np.stack([np.zeros(B, np.int32), 1 + np.arange(B, dtype=np.int32)], axis=1)
     desc = W.BatchDesc(np.full(B, CTX, np.int32), np.full(B, GAMMA, np.int32), to_dev(pt), T,
                        np.arange(B, dtype=np.uint32))

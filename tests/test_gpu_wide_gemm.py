@@ -1,0 +1,46 @@
+"""The wide-output projections at the stated bf16 bound.
+
+gate/up and the LM head run the 64-column weight-ring GEMM once their output is at least
+16384 columns wide, which the 8B / 70B shapes always are and the small test models never
+were.  This model makes both wide at a width the oracle recomputes in seconds: d_model
+512, 8 query heads on 2 kv heads of 64, d_ff 8192 (gate/up 16384 columns), vocabulary
+32768, bf16, 2 layers.  At d_model 512 the gate/up projection is also split over K (two
+ranges summed in fixed order), the LM head is not.
+
+Cases: 44 rows (one row block of the GEMMs) and 510 rows (two row blocks of 256, each
+re-streaming the weights).  Checks: logits within 2e-2 max-abs of the oracle, every
+written K/V value within one bf16 ulp, untouched slots bit-identical, decisions on the
+GPU's own logits bit-exact except flagged near-ties.
+"""
+import numpy as np
+import pytest
+
+import wisp_inputs as wi
+from oracle import fixtures as fx
+from gpu_harness import Workload, check_decisions_on_gpu_logits, check_written, gpu_model, log, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+WIDE_BF16 = wi.ModelShape("wide-bf16", 2, 512, 8, 2, 64, 8192, 32768, "bf16", 10000.0)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("B", [8, 30], ids=["44rows", "510rows"])
+def test_wide_projections_match_the_oracle(B):
+    r = np.random.default_rng(8192 + B)
+    ctx = r.integers(0, 64, size=B).astype(np.int32)
+    # 8 requests of 36 drafts in all: 44 rows; 30 requests of 16 drafts: 510 rows
+    gamma = np.array([7, 1, 5, 3, 6, 4, 2, 8] if B == 8 else [16] * B, np.int32)
+    mix = wi.custom_mix(WIDE_BF16, ctx, gamma, kv_source="prefill", name=f"wide-{B}", t_draft=1.0,
+                        sigma=0.5)
+    log(f"{WIDE_BF16.name}: B={B} M={mix.M} ctx={ctx.tolist()} gamma={gamma.tolist()}")
+    wl = Workload(mix, fx.host_model(WIDE_BF16))
+    acc, out, logits, pools = run_gpu(gpu_model(WIDE_BF16), wl)
+    d = np.abs(logits - wl.logits_ref)
+    log(f"  logits max-abs error {d.max():.3e}, mean {d.mean():.3e} (|ref| max {np.abs(wl.logits_ref).max():.2f})")
+    assert d.max() <= 2e-2
+    worst = check_written(pools, wl.pools_ref, wl.pools0, wl.pt, mix.ctx_len, mix.rows, WIDE_BF16.head_dim, True)
+    log(f"  written K/V: worst error / one bf16 ulp {worst:.2f}")
+    n_id, m_id = check_decisions_on_gpu_logits(acc, out, logits, wl.tokens, wl.q, mix.gamma, 1.0, wl.seed,
+                                               req_id=mix.req_id)
+    log(f"  on the GPU's own logits: {n_id} decisions, {m_id} flagged mismatches")

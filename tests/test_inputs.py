@@ -64,9 +64,9 @@ def test_workload_mixes():
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_context_kv_placement_agrees_slot_by_slot(dtype):
-    """The oracle's host placement and the device-side fill put every context position's
-    K and V at the slot the page table and page layout name (checked one slot at a time),
-    and touch nothing else."""
+    """The oracle's host placement (slot-major pages) and the device-side fill (the
+    library's page order) put every context position's K and V at the slot the page table
+    and the respective layout name (checked one slot at a time), and touch nothing else."""
     import torch
     from oracle import fixtures as fx
     shape = wi.ModelShape("place", 2, 256, 4, 2, 64, 512, 1024, dtype, 1e4)
@@ -78,17 +78,22 @@ def test_context_kv_placement_agrees_slot_by_slot(dtype):
     dev_k = torch.zeros(shape.n_layers, nb, shape.n_kv_heads, 16 * shape.head_dim, dtype=tdt)
     dev_v = torch.zeros_like(dev_k)
     wi.fill_kv_pool(dev_k, dev_v, mix, pt)
-    ref = fx.empty_pools(shape, nb)
-    kidx, vidx = wi.k_page_index(shape.head_dim), wi.v_page_index(shape.head_dim)
+    hd = shape.head_dim
+    ref = fx.empty_pools(shape, nb)          # slot-major
+    ref_dev = fx.empty_pools(shape, nb)      # the library's page order
+    kidx, vidx = wi.k_page_index(hd), wi.v_page_index(hd)
     for i in range(mix.B):
         n = int(mix.ctx_len[i])
         for l in range(shape.n_layers):
-            K, V = wi.kv_values(mix.seed, l, i, 0, n, shape.n_kv_heads, shape.head_dim, "cpu", tdt)
+            K, V = wi.kv_values(mix.seed, l, i, 0, n, shape.n_kv_heads, hd, "cpu", tdt)
             K, V = fx._to_storage(K, shape), fx._to_storage(V, shape)
             for t in range(n):
                 for h in range(shape.n_kv_heads):
-                    ref[0][l, pt[i, t // 16], h, kidx[t % 16]] = K[t, h]
-                    ref[1][l, pt[i, t // 16], h, vidx[t % 16]] = V[t, h]
+                    b, sl = pt[i, t // 16], t % 16
+                    ref[0][l, b, h, sl * hd:(sl + 1) * hd] = K[t, h]
+                    ref[1][l, b, h, sl * hd:(sl + 1) * hd] = V[t, h]
+                    ref_dev[0][l, b, h, kidx[sl]] = K[t, h]
+                    ref_dev[1][l, b, h, vidx[sl]] = V[t, h]
     for w, dev in ((0, dev_k), (1, dev_v)):
         np.testing.assert_array_equal(host[w], ref[w])
-        np.testing.assert_array_equal(fx._to_storage(dev, shape), ref[w])
+        np.testing.assert_array_equal(fx._to_storage(dev, shape), ref_dev[w])

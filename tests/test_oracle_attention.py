@@ -36,7 +36,7 @@ def _case(B, n_q, n_kv, hd, seed, bf16):
     else:
         kd, vd = kd.astype(np.float32).astype(np.float64), vd.astype(np.float32).astype(np.float64)
         kp, vp = kd.astype(np.float32), vd.astype(np.float32)
-    kp, vp = wi.pages_from_slots(kp, "k"), wi.pages_from_slots(vp, "v")
+    kp, vp = kp.reshape(n_blocks, n_kv, PAGE * hd), vp.reshape(n_blocks, n_kv, PAGE * hd)   # slot-major pages
     M = int(n_new.sum())
     q = rng.standard_normal((M, n_q, hd))
     return ctx, n_new, pt, kd, vd, kp, vp, q

@@ -127,9 +127,9 @@ def _dense_forward(shape, layers, glob, pools, pt, ctx, n_new, toks):
     hd = shape.head_dim
     kp = torch.from_numpy(pools[0].astype(np.int32) << 16).view(torch.float32) if bf16 else torch.from_numpy(pools[0])
     vp = torch.from_numpy(pools[1].astype(np.int32) << 16).view(torch.float32) if bf16 else torch.from_numpy(pools[1])
-    # pages -> [layer][block][kv][slot][dim]
-    kp = wi.slots_from_pages(kp.to(torch.float64), "k", hd)
-    vp = wi.slots_from_pages(vp.to(torch.float64), "v", hd)
+    # slot-major pages -> [layer][block][kv][slot][dim]
+    kp = kp.to(torch.float64).reshape(kp.shape[:3] + (16, hd))
+    vp = vp.to(torch.float64).reshape(vp.shape[:3] + (16, hd))
     out = []
     off = 0
     for i in range(len(ctx)):
@@ -181,3 +181,47 @@ def test_dense_library_reformulation(setup):
         err = np.abs(got - want).max()
         assert err < 2e-2, err
         assert np.mean(np.abs(got - want) < 1e-5) > 0.5
+
+
+# ------------------------------------------------------------------------------------
+# the fp32-accumulation mode (a second correct rounding order)
+# ------------------------------------------------------------------------------------
+def test_fp32_sums_stay_within_the_textbook_bound():
+    """A projection with fp32 sums in natural order: |fl(sum) - sum| <= gamma_n * sum |x_k w_k|
+    with gamma_n = n u / (1 - n u), u = 2^-24 (the standard bound for recursive summation
+    of exact products: the products of bf16-valued operands are exact in fp32).  The fp64
+    mode agrees with numpy's fp64 matmul."""
+    rng = np.random.default_rng(3)
+    n = 4096
+    W_ = oracle.round_bf16(rng.standard_normal((64, n)) * 0.02).astype(np.float32)
+    x = oracle.round_bf16(rng.standard_normal((5, n)))
+    y64 = oracle.linear_apply(W_, x)
+    y32 = oracle.linear_apply(W_, x, acc32=True)
+    np.testing.assert_allclose(y64, x @ W_.astype(np.float64).T, rtol=1e-12, atol=1e-12)
+    u = 2.0 ** -24
+    gam = n * u / (1 - n * u)
+    bound = gam * (np.abs(x) @ np.abs(W_.astype(np.float64)).T)
+    assert np.all(np.abs(y32 - y64) <= bound)
+    assert np.any(y32 != y64)                          # the sums really are fp32
+    assert np.all(y32 == y32.astype(np.float32))       # and the results fp32 values
+
+
+@pytest.mark.parametrize("shape", [wi.TINY, MINI_BF16], ids=["fp32", "bf16"])
+def test_fp32_accumulation_mode_stays_near_the_fp64_forward(shape):
+    """fp32 model: the fp32-summed forward is within 1e-5 relative per row of the fp64 one.
+    bf16 model: within the bf16 logits bound, and not identical (the rounding points see
+    different sums, which is what the mode is for)."""
+    mix = wi.custom_mix(shape, [37, 16, 0, 50], [4, 2, 3, 0], kv_source="prefill", name="acc32")
+    model = fx.host_model(shape)
+    pt, nb = wi.page_table(mix)
+    pools = fx.empty_pools(shape, nb)
+    fx.prefill_context(model, mix, pools, pt)
+    toks = np.random.default_rng(2).integers(0, shape.vocab, size=mix.M).astype(np.int32)
+    a = oracle.forward(model, pools[0].copy(), pools[1].copy(), pt, mix.ctx_len, mix.rows, toks)
+    b = oracle.forward(model, pools[0].copy(), pools[1].copy(), pt, mix.ctx_len, mix.rows, toks, acc32=True)
+    if shape.dtype == "f32":
+        rel = np.abs(a - b).max(axis=1) / np.abs(a).max(axis=1)
+        assert rel.max() <= 1e-5, rel.max()
+    else:
+        d = np.abs(a - b)
+        assert d.max() <= 2e-2 and d.max() > 0, d.max()

@@ -114,19 +114,3 @@ def test_native_entry_points_reject_bad_arguments():
     m.n_in = 4
     assert lib.wisp_reject_predict(C.byref(m), None, 0, None, None) == W.WISP_OK
     assert lib.wisp_reject_predict(C.byref(m), None, 1, None, None) == W.WISP_E_INVALID
-
-
-def test_trace_labels_and_auc():
-    """App. B's labels: accepted drafts are 1, the first rejection 0, later positions out;
-    a fully accepted window has no 0.  The rank AUC agrees with scikit-learn's."""
-    import sklearn.metrics
-    from paper_2601_11652_amd.predictor import _auc, _labelled
-    f = lambda v: np.array([v], np.float32)   # noqa: E731
-    trace = [(7, j, f(10 + j)) for j in range(4)] + [(9, j, f(20 + j)) for j in range(3)]
-    X, y = _labelled(trace, [9, 7], accept_len=np.array([3, 1]), drafted=[3, 4])
-    assert [float(x[0]) for x in X] == [10, 11, 20, 21, 22] and y == [1.0, 0.0, 1.0, 1.0, 1.0]
-    rng = np.random.default_rng(1)
-    lab = rng.random(500) < 0.6
-    sc = rng.standard_normal(500) + lab
-    sc[:50] = np.round(sc[:50])                       # some ties
-    assert abs(_auc(sc, lab) - sklearn.metrics.roc_auc_score(lab, sc)) < 1e-12
