@@ -364,12 +364,18 @@ static void residual_add(const orc_model *m, double *h, const double *t, int64_t
   for (int64_t e = 0; e < n; e++) h[e] = m->acc32 ? (double)((float)h[e] + (float)t[e]) : h[e] + t[e];
 }
 
-/* RMSNorm: x * g / sqrt(mean(x^2) + eps). */
+/* RMSNorm: x * g / sqrt(mean(x^2) + eps); acc32 sums the squares in fp32. */
 static void rmsnorm(const orc_model *m, const void *g, const double *h, double *x, int rows) {
   int d = m->d;
   for (int r = 0; r < rows; r++) {
     double ss = 0.0;
-    for (int k = 0; k < d; k++) ss += h[(int64_t)r * d + k] * h[(int64_t)r * d + k];
+    float ss32 = 0.0f;
+    for (int k = 0; k < d; k++) {
+      const double v = h[(int64_t)r * d + k];
+      ss += v * v;
+      ss32 += (float)v * (float)v;
+    }
+    if (m->acc32) ss = ss32;
     double inv = 1.0 / sqrt(ss / d + m->eps);
     for (int k = 0; k < d; k++)
       x[(int64_t)r * d + k] = act_round(m, h[(int64_t)r * d + k] * inv * wval(m, g, k));

@@ -65,26 +65,44 @@ def bf16_ulp(x: np.ndarray) -> np.ndarray:
     return 2.0 ** (np.floor(np.log2(a)) - 7)
 
 
+def kv_bound(ref: np.ndarray, hd: int) -> np.ndarray:
+    """Two bf16 ulps at the scale of each K/V value, the scale being its head vector's
+    largest magnitude (one token's K or V row of one kv head): one ulp for the rounding of
+    the stored value itself (the two sides may round to either neighbour), one for the
+    rounding flips of earlier values that reach its sum.  A sum's rounding error scales with
+    its terms, not with its result, so a value near a cancelling zero carries the error of
+    its vector's scale.  ref: slot-major pools [..., 16 * hd]."""
+    v = np.abs(ref).reshape(ref.shape[:-1] + (wi.PAGE, hd))
+    scale = v.max(axis=-1, keepdims=True) + 0.0 * v
+    return 2.0 * bf16_ulp(scale).reshape(ref.shape)
+
+
 def check_written(pools_gpu, pools_ref, pools_before, page_table, ctx_len, n_new, hd: int, bf16: bool,
-                  f32_atol: float = 1e-4, floor=None):
+                  f32_atol: float = 1e-4, pools_ref32=None):
     """K/V written at the new positions match the oracle's, every other slot is untouched
-    bit for bit.  bf16: within one bf16 ulp of the oracle's value (two correct fp32
-    accumulation orders may round a value on either side of a bf16 boundary), or, where
-    `floor` gives a per-layer pair (K, V) of the oracle's own floor, within twice it.  fp32:
-    within f32_atol."""
+    bit for bit.  bf16: each value within max(two bf16 ulps at its scale (kv_bound), twice
+    the layer's floor), the floor being max |oracle with fp32 sums - oracle with fp64 sums|
+    over the layer's written K (or V) values (pools_ref32: the fp32-sum oracle's pools).
+    Two correct accumulation orders round some values on different sides of a bf16 boundary,
+    and each layer's flips move the next layer's sums.  fp32: within f32_atol."""
     worst = 0.0
     for w in range(2):
         g = storage_to_f64(pools_gpu[w])
         r = storage_to_f64(pools_ref[w])
+        r32 = storage_to_f64(pools_ref32[w]) if pools_ref32 is not None else None
         before = storage_to_f64(pools_before[w])
         written = written_mask(g.shape, page_table, ctx_len, n_new, hd)
+        ulp = kv_bound(r, hd) if bf16 else None
         for l in range(g.shape[0]):
             gl, rl = g[l][written[l]], r[l][written[l]]
             if gl.size == 0:
                 continue
-            bound = bf16_ulp(rl) if bf16 else np.full(rl.shape, f32_atol)
-            if floor is not None:
-                bound = np.maximum(bound, 2.0 * floor[l][w])
+            if bf16:
+                bound = ulp[l][written[l]]
+                if r32 is not None:
+                    bound = np.maximum(bound, 2.0 * np.abs(r32[l][written[l]] - rl).max())
+            else:
+                bound = np.full(rl.shape, f32_atol)
             ratio = float((np.abs(gl - rl) / bound).max())
             assert ratio <= 1.0, ("KV"[w], l, ratio, float(np.abs(gl - rl).max()))
             worst = max(worst, ratio)
@@ -125,10 +143,15 @@ class Workload:
         self.q = (np.concatenate([qs[i] for i in range(mix.B)]).astype(np.float32)
                   if S else np.zeros((0, s.vocab), np.float32))
         self.seed = wi.verify_seed(mix)
-        # reference forward on the pre-step pools
+        # reference forward on the pre-step pools (bf16: also with fp32 sums, the floor)
         self.pools_ref = (self.pools0[0].copy(), self.pools0[1].copy())
         self.logits_ref = oracle.forward(model, self.pools_ref[0], self.pools_ref[1], self.pt, mix.ctx_len,
                                          mix.rows, self.tokens)
+        self.pools_ref32 = None
+        if s.dtype == "bf16":
+            self.pools_ref32 = (self.pools0[0].copy(), self.pools0[1].copy())
+            self.logits_ref32 = oracle.forward(model, self.pools_ref32[0], self.pools_ref32[1], self.pt,
+                                               mix.ctx_len, mix.rows, self.tokens, acc32=True)
 
 
 def run_gpu(gm: W.GpuModel, wl: Workload):

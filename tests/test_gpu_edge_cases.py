@@ -37,7 +37,7 @@ MINI_BF16 = wi.ModelShape("mini-bf16-gqa", 2, 256, 8, 2, 64, 512, 1024, "bf16", 
 def _check_written(wl, pools_gpu):
     mix = wl.mix
     check_written(pools_gpu, wl.pools_ref, wl.pools0, wl.pt, mix.ctx_len, mix.rows, mix.shape.head_dim,
-                  mix.shape.dtype == "bf16")
+                  mix.shape.dtype == "bf16", pools_ref32=wl.pools_ref32)
 
 
 def _run_case(shape, ctx, gamma, logit_check, u_margin=1e-3):

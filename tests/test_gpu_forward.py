@@ -23,7 +23,7 @@ def _check_pools(wl, pools_gpu):
     """New positions match the oracle's writes; every other slot is untouched."""
     mix = wl.mix
     check_written(pools_gpu, wl.pools_ref, wl.pools0, wl.pt, mix.ctx_len, mix.rows, mix.shape.head_dim,
-                  mix.shape.dtype == "bf16")
+                  mix.shape.dtype == "bf16", pools_ref32=wl.pools_ref32)
 
 
 @pytest.mark.parametrize("T", [1.0, 0.0])

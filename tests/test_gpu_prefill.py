@@ -55,9 +55,14 @@ def _case(shape, ctx, pre, gam, name, T=1.0):
     pools_ref = (pools0[0].copy(), pools0[1].copy())
     n_new = (pre + gam + 1).astype(np.int32)
     logits_all = oracle.forward(model, pools_ref[0], pools_ref[1], pt, ctx, n_new, tokens)
+    pools_ref32 = None
+    if shape.dtype == "bf16":      # the fp32-sum oracle: the floor of the K/V check
+        pools_ref32 = (pools0[0].copy(), pools0[1].copy())
+        oracle.forward(model, pools_ref32[0], pools_ref32[1], pt, ctx, n_new, tokens, acc32=True)
     ends = np.cumsum(n_new)
     logits_ref = np.concatenate([logits_all[ends[i] - gam[i] - 1:ends[i]] for i in range(B)])
-    return dict(mix=mix, ctx=ctx, pre=pre, gam=gam, pt=pt, pools0=pools0, pools_ref=pools_ref, tokens=tokens,
+    return dict(mix=mix, ctx=ctx, pre=pre, gam=gam, pt=pt, pools0=pools0, pools_ref=pools_ref,
+                pools_ref32=pools_ref32, tokens=tokens,
                 vtokens=vtokens, q=q, seed=seed, logits_ref=logits_ref, T=T)
 
 
@@ -82,7 +87,7 @@ def _run(shape, c):
 
 def _check_kv(shape, c, pools):
     worst = check_written(pools, c["pools_ref"], c["pools0"], c["pt"], c["ctx"], c["pre"] + c["gam"] + 1,
-                          shape.head_dim, shape.dtype == "bf16")
+                          shape.head_dim, shape.dtype == "bf16", pools_ref32=c["pools_ref32"])
     log(f"  new K/V slots: worst error / bound {worst:.2f}")
 
 

@@ -9,8 +9,9 @@ ranges summed in fixed order), the LM head is not.
 
 Cases: 44 rows (one row block of the GEMMs) and 510 rows (two row blocks of 256, each
 re-streaming the weights).  Checks: logits within 2e-2 max-abs of the oracle, every
-written K/V value within one bf16 ulp, untouched slots bit-identical, decisions on the
-GPU's own logits bit-exact except flagged near-ties.
+written K/V value within max(two bf16 ulps at its head vector's scale, twice the oracle's floor of its
+layer), untouched slots bit-identical, decisions on the GPU's own logits bit-exact except
+flagged near-ties.
 """
 import numpy as np
 import pytest
@@ -39,8 +40,9 @@ def test_wide_projections_match_the_oracle(B):
     d = np.abs(logits - wl.logits_ref)
     log(f"  logits max-abs error {d.max():.3e}, mean {d.mean():.3e} (|ref| max {np.abs(wl.logits_ref).max():.2f})")
     assert d.max() <= 2e-2
-    worst = check_written(pools, wl.pools_ref, wl.pools0, wl.pt, mix.ctx_len, mix.rows, WIDE_BF16.head_dim, True)
-    log(f"  written K/V: worst error / one bf16 ulp {worst:.2f}")
+    worst = check_written(pools, wl.pools_ref, wl.pools0, wl.pt, mix.ctx_len, mix.rows, WIDE_BF16.head_dim, True,
+                          pools_ref32=wl.pools_ref32)
+    log(f"  written K/V: worst error / bound {worst:.2f}")
     n_id, m_id = check_decisions_on_gpu_logits(acc, out, logits, wl.tokens, wl.q, mix.gamma, 1.0, wl.seed,
                                                req_id=mix.req_id)
     log(f"  on the GPU's own logits: {n_id} decisions, {m_id} flagged mismatches")
