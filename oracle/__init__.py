@@ -6,8 +6,10 @@ library (``paper_2601_11652_amd``) never does, and the two share no code.
 
 The arithmetic lives in plain C (``wisp_oracle.c``, fp64 forward / fp32 acceptance)
 and is reached through ctypes.  The forward also has an fp32-accumulation mode
-(``acc32``: every sum in fp32, natural index order), a second correct rounding order
-whose distance from the fp64 result measures the bf16 contract's own noise floor.
+(``acc32``: every sum in fp32, natural index order, and in bf16 models the attention
+weights rounded to bf16 before they weight the values, as a bf16 matrix-core product
+takes them), a second correct rounding order whose distance from the fp64 result
+measures the bf16 contract's own noise floor.
 KV pools are natural ``[n_layers][n_blocks][n_kv][16][head_dim]`` arrays (slot-major
 pages); the GPU library's page order is a separate interface layout, converted at the
 test boundary.  What each function follows in the paper:

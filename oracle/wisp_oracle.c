@@ -415,7 +415,10 @@ static int64_t kv_index(int n_kv, int hd, int block, int kvh, int slot, int dim)
 /* Causal attention of the new rows over each request's paged KV (one layer).
  * q: [M][n_q][hd]; out: [M][n_q][hd].  Row j of request i sits at position
  * ctx_len[i] + j and sees keys 0 .. ctx_len[i] + j.  acc32: the dot products, the
- * softmax denominator and the weighted sum of values accumulate in fp32. */
+ * softmax denominator and the weighted sum of values accumulate in fp32, and in bf16
+ * mode the weights exp(s - max) are rounded to bf16 first (the operand precision of a
+ * bf16 matrix-core product of weights and values), the denominator summing the rounded
+ * weights. */
 int orc_paged_attention(int n_q, int n_kv, int hd, int bf16, int acc32, const void *k_pool,
                         const void *v_pool, const int32_t *page_table, int pt_stride, int B,
                         const int32_t *ctx_len, const int32_t *n_new, const double *q, double *out) {
@@ -454,6 +457,7 @@ int orc_paged_attention(int n_q, int n_kv, int hd, int bf16, int acc32, const vo
     float den32 = 0.0f;
     for (int t = 0; t <= pos; t++) {
       s[t] = exp(s[t] - mx);
+      if (acc32 && bf16) s[t] = round_bf16(s[t]);
       den += s[t];
       den32 += (float)s[t];
     }
