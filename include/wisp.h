@@ -185,6 +185,28 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * wisp_verify for callers that cannot allocate: code under HIP graph capture, serving loops
+ * and harnesses that forbid hipMalloc.  It takes no workspace: the step's scratch is a
+ * static array of WISP_NOALLOC_SCRATCH_BYTES that every GPU the library runs on holds
+ * until the process ends, and the batch descriptor reaches the device as kernel arguments
+ * (no pinned staging).  It calls no hipMalloc, hipFree or other allocating HIP routine (its
+ * host-side planning uses ordinary heap memory).  Same inputs, outputs, kernels and results
+ * as wisp_verify, plus:
+ *   fault   DEVICE int32 [1] or NULL: device-side input faults are OR-ed into it (1: a token
+ *           id outside [0, vocab), 2: a block id outside [0, n_blocks)); the caller zeroes it
+ *           and reads it after synchronising.  With NULL, faults go unreported.
+ * A batch whose scratch (wisp_workspace_size, plus wisp_logits_workspace_size when
+ * target_logits is NULL) exceeds WISP_NOALLOC_SCRATCH_BYTES returns WISP_E_WORKSPACE before
+ * any GPU work.  Every call on one GPU shares that GPU's array: calls that overlap on it
+ * (other streams, other threads) race and must be serialised by the caller.
+ */
+#define WISP_NOALLOC_SCRATCH_BYTES (128u << 20)
+wisp_status wisp_verify_noalloc(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                                const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
+                                int32_t *accept_len, int32_t *out_tokens, float *target_logits, int32_t *fault,
+                                void *stream);
+
+/*
  * The acceptance stage alone (Sec. 2.4, Eq. (1)-(3) with the residual), on given
  * logits: the same kernels and random streams as wisp_verify's last stage.
  * Uses desc->B, gamma, req_id, temperature only.  logits DEVICE fp32 [M][vocab].

@@ -43,7 +43,7 @@ EXPORTS = ("wisp_workspace_size", "wisp_logits_workspace_size", "wisp_accept_wor
            "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule", "wisp_kvm_create",
            "wisp_kvm_destroy", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit", "wisp_kvm_release",
            "wisp_kvm_get_stats", "wisp_draft_stats_workspace_size", "wisp_draft_stats", "wisp_reject_predict",
-           "wisp_gemm_plan")
+           "wisp_gemm_plan", "wisp_verify_noalloc")
 
 
 class WispError(RuntimeError):
@@ -125,6 +125,8 @@ def _load():
     L.wisp_pack_linear.argtypes = [_VP, _VP, C.c_int32, C.c_int32, C.c_int32, _VP]
     L.wisp_verify.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
                               _VP, _VP, C.c_uint64, _VP, _VP, _VP, _VP, C.c_size_t, _VP]
+    L.wisp_verify_noalloc.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
+                                      _VP, _VP, C.c_uint64, _VP, _VP, _VP, _VP, _VP]
     L.wisp_accept.argtypes = [C.POINTER(wisp_batch_desc), C.c_int32, _VP, _VP, _VP, C.c_uint64, _VP,
                               _VP, _VP, C.c_size_t, _VP]
     L.wisp_attention.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
@@ -154,7 +156,7 @@ def _load():
     L.wisp_draft_stats_workspace_size.restype = C.c_size_t
     L.wisp_draft_stats.argtypes = [_VP, C.c_int32, C.c_int32, C.c_int64, C.c_float, _VP, _VP, C.c_size_t, _VP]
     L.wisp_reject_predict.argtypes = [C.POINTER(wisp_reject_mlp), _VP, C.c_int32, _VP, _VP]
-    for name in ("wisp_pack_linear", "wisp_verify", "wisp_accept", "wisp_attention", "wisp_uniform",
+    for name in ("wisp_pack_linear", "wisp_verify", "wisp_verify_noalloc", "wisp_accept", "wisp_attention", "wisp_uniform",
                  "wisp_check", "wisp_gemm_plan", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
                  "wisp_schedule", "wisp_kvm_create", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit",
                  "wisp_kvm_release", "wisp_kvm_get_stats", "wisp_draft_stats", "wisp_reject_predict"):
@@ -408,6 +410,23 @@ def wisp_verify(model: wisp_model, kv: KVPool, desc: BatchDesc, tokens, draft_pr
                         _dev(accept_len, "accept_len", desc.B, dtype=_i32()),
                         _dev(out_tokens, "out_tokens", desc.M, dtype=_i32()), logits, *_ws(workspace),
                         _stream(stream)))
+
+
+def wisp_verify_noalloc(model: wisp_model, kv: KVPool, desc: BatchDesc, tokens, draft_probs, rng_seed: int,
+                        accept_len, out_tokens, target_logits, fault=None, stream=None):
+    """wisp_verify without a workspace (the library's static per-device scratch); `fault`
+    (device int32 [1] or None) accumulates device-side input faults."""
+    _check_desc(desc)
+    _check_kv(model, kv, model.n_layers)
+    V = model.vocab
+    probs = _dev(draft_probs, "draft_probs", desc.S * V, dtype=_f32()) if desc.S > 0 else _ptr(draft_probs)
+    logits = None if target_logits is None else _dev(target_logits, "target_logits", desc.M * V, dtype=_f32())
+    flt = None if fault is None else _dev(fault, "fault", 1, dtype=_i32())
+    _ok(lib.wisp_verify_noalloc(C.byref(model), C.byref(kv.c), C.byref(desc.c),
+                                _dev(tokens, "tokens", desc.rows, dtype=_i32()), probs, rng_seed & ((1 << 64) - 1),
+                                _dev(accept_len, "accept_len", desc.B, dtype=_i32()),
+                                _dev(out_tokens, "out_tokens", desc.M, dtype=_i32()), logits, flt,
+                                _stream(stream)))
 
 
 def wisp_accept(desc: BatchDesc, vocab: int, logits, tokens, draft_probs, rng_seed: int, accept_len,

@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -436,7 +437,7 @@ SamplerScratch sampler_scratch(const Plan &p, char *ws) {
   return sc;
 }
 
-StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_blocks) {
+StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_blocks, int *err = nullptr) {
   const int32_t *base = reinterpret_cast<const int32_t *>(ws + p.w_desc);
   StepDesc sd;
   sd.off = base + p.i_off;
@@ -450,7 +451,7 @@ StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_bloc
   sd.page_table = d->kv_page_table;
   sd.pt_stride = d->pt_stride;
   sd.n_blocks = n_blocks;
-  sd.err = reinterpret_cast<int *>(ws + p.w_err);
+  sd.err = err ? err : reinterpret_cast<int *>(ws + p.w_err);
   return sd;
 }
 
@@ -567,6 +568,115 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
 
 }  // namespace
 
+namespace {
+
+// validation shared by the two verification entry points
+wisp_status check_verify(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                         const int32_t *tokens, const int32_t *accept_len, const int32_t *out_tokens) {
+  wisp_status st;
+  if ((st = check_model(model, true)) != WISP_OK) return st;
+  if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
+  if (desc->B == 0) return WISP_OK;
+  if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
+  if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
+  if (kv->n_blocks <= 0) return fail(WISP_E_INVALID, "n_blocks must be positive");
+  if (!tokens || !accept_len || !out_tokens) return fail(WISP_E_INVALID, "NULL tokens / outputs");
+  return WISP_OK;
+}
+
+wisp_status plan_verify(Plan &p, const wisp_model *model, const wisp_batch_desc *desc, const float *draft_probs) {
+  wisp_status st;
+  if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
+  if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
+  if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
+  return WISP_OK;
+}
+
+// the step's kernel sequence on a planned, uploaded workspace `ws`; `err` (or NULL: the
+// workspace's own record) receives the device-side input faults
+wisp_status run_verify(const Plan &p, const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                       const int32_t *tokens, const float *draft_probs, uint64_t rng_seed, int32_t *accept_len,
+                       int32_t *out_tokens, float *target_logits, char *ws, int *err, hipStream_t s) {
+  wisp_status st;
+  StepDesc sd = step_desc(p, ws, desc, kv->n_blocks, err);
+  if (p.bf16)
+    st = run_forward<uint16_t>(p, model, kv, sd, ws, tokens, target_logits, s);
+  else
+    st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
+  if (st != WISP_OK) return st;
+  // the acceptance sees the verification rows only: row offsets over them, and (with
+  // prompt rows present) their tokens gathered into a compact array
+  StepDesc sv = sd;
+  sv.off = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_voff;
+  const int32_t *vtok = tokens;
+  if (p.prefill) {
+    int32_t *g = reinterpret_cast<int32_t *>(ws + p.w_vtok);
+    gather_ints(tokens, reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow, p.Mv, g, s);
+    vtok = g;
+  }
+  ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
+  sampler(sv, p.B, p.Mv, p.V, target_logits, vtok, draft_probs, desc->temperature, rng_seed,
+          sampler_scratch(p, ws), accept_len, out_tokens, s);
+  return hip_check("sampler launch");
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------------
+// Scratch of the allocation-free entry point: one static array, of which every GPU the
+// library runs on holds its own copy (at its own address, looked up once per device).
+// Host code never uses the array's name as an address, only the looked-up pointer.
+// ------------------------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[WISP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+wisp_status noalloc_scratch(char **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(WISP_E_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return fail(WISP_E_UNSUPPORTED, "device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(WISP_E_HIP, "scratch address on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = static_cast<char *>(g_scratch_ptr[dev]);
+  return WISP_OK;
+}
+
+// The descriptor block reaches the device as kernel arguments, a few KB per launch: no
+// pinned staging buffer and no host copy that must outlive the call.
+constexpr int kDescChunkInts = 960;
+struct DescChunk {
+  int32_t n;
+  int32_t v[kDescChunkInts];
+};
+
+__global__ void put_desc_kernel(DescChunk c, int32_t *__restrict__ dst) {
+  for (int i = threadIdx.x; i < c.n; i += blockDim.x) dst[i] = c.v[i];
+}
+
+wisp_status upload_by_arguments(const Plan &p, char *ws, hipStream_t s) {
+  int32_t *dst = reinterpret_cast<int32_t *>(ws + p.w_desc);
+  const size_t n = p.host.size();
+  DescChunk c;
+  for (size_t o = 0; o < n; o += kDescChunkInts) {
+    c.n = (int32_t)std::min<size_t>(kDescChunkInts, n - o);
+    std::memcpy(c.v, p.host.data() + o, (size_t)c.n * sizeof(int32_t));
+    launch(put_desc_kernel, 1, 256, 0, s, c, dst + o);
+  }
+  return hip_check("descriptor upload");
+}
+
+}  // namespace
+
 namespace wisp {
 // lets the host-only sources (the scheduler, the KV manager) report through wisp_last_error
 wisp_status report_error(wisp_status st, const char *msg) { return fail(st, "%s", msg); }
@@ -635,18 +745,11 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
                         void *workspace, size_t workspace_bytes, void *stream) {
   return guarded("wisp_verify", [&]() -> wisp_status {
     wisp_status st;
-    if ((st = check_model(model, true)) != WISP_OK) return st;
-    if ((st = check_desc(desc, true, true)) != WISP_OK) return st;
+    if ((st = check_verify(model, kv, desc, tokens, accept_len, out_tokens)) != WISP_OK) return st;
     if (desc->B == 0) return WISP_OK;
-    if (!kv || !kv->k_pool || !kv->v_pool) return fail(WISP_E_INVALID, "KV pools are NULL");
-    if (kv->page_size != WISP_PAGE) return fail(WISP_E_UNSUPPORTED, "page_size must be %d", WISP_PAGE);
-    if (kv->n_blocks <= 0) return fail(WISP_E_INVALID, "n_blocks must be positive");
-    if (!tokens || !accept_len || !out_tokens || !workspace)
-      return fail(WISP_E_INVALID, "NULL tokens / outputs / workspace");
+    if (!workspace) return fail(WISP_E_INVALID, "NULL workspace");
     Plan p;
-    if ((st = make_plan(p, model, desc, true)) != WISP_OK) return st;
-    if (p.S > 0 && !draft_probs) return fail(WISP_E_INVALID, "draft_probs is NULL");
-    if (!p.bf16 && p.max_tokens > 32768) return fail(WISP_E_UNSUPPORTED, "fp32 path supports <= 32768 tokens per request");
+    if ((st = plan_verify(p, model, desc, draft_probs)) != WISP_OK) return st;
     // without a caller buffer the logits live in the workspace, after everything else
     const size_t need = p.total + (target_logits ? 0 : align256((size_t)p.Mv * (size_t)p.V * sizeof(float)));
     if (workspace_bytes < need)
@@ -655,28 +758,32 @@ wisp_status wisp_verify(const wisp_model *model, const wisp_kv *kv, const wisp_b
     char *ws = (char *)workspace;
     if (!target_logits) target_logits = reinterpret_cast<float *>(ws + p.total);
     if ((st = upload(p, ws, s)) != WISP_OK) return st;
-    StepDesc sd = step_desc(p, ws, desc, kv->n_blocks);
-    if (p.bf16)
-      st = run_forward<uint16_t>(p, model, kv, sd, ws, tokens, target_logits, s);
-    else
-      st = run_forward<float>(p, model, kv, sd, ws, tokens, target_logits, s);
-    if (st != WISP_OK) return st;
-    {
-      // the acceptance sees the verification rows only: row offsets over them, and (with
-      // prompt rows present) their tokens gathered into a compact array
-      StepDesc sv = sd;
-      sv.off = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_voff;
-      const int32_t *vtok = tokens;
-      if (p.prefill) {
-        int32_t *g = reinterpret_cast<int32_t *>(ws + p.w_vtok);
-        gather_ints(tokens, reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow, p.Mv, g, s);
-        vtok = g;
-      }
-      ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
-      sampler(sv, p.B, p.Mv, p.V, target_logits, vtok, draft_probs, desc->temperature, rng_seed,
-              sampler_scratch(p, ws), accept_len, out_tokens, s);
-    }
-    return hip_check("sampler launch");
+    return run_verify(p, model, kv, desc, tokens, draft_probs, rng_seed, accept_len, out_tokens, target_logits,
+                      ws, nullptr, s);
+  });
+}
+
+wisp_status wisp_verify_noalloc(const wisp_model *model, const wisp_kv *kv, const wisp_batch_desc *desc,
+                                const int32_t *tokens, const float *draft_probs, uint64_t rng_seed,
+                                int32_t *accept_len, int32_t *out_tokens, float *target_logits, int32_t *fault,
+                                void *stream) {
+  return guarded("wisp_verify_noalloc", [&]() -> wisp_status {
+    wisp_status st;
+    if ((st = check_verify(model, kv, desc, tokens, accept_len, out_tokens)) != WISP_OK) return st;
+    if (desc->B == 0) return WISP_OK;
+    Plan p;
+    if ((st = plan_verify(p, model, desc, draft_probs)) != WISP_OK) return st;
+    const size_t need = p.total + (target_logits ? 0 : align256((size_t)p.Mv * (size_t)p.V * sizeof(float)));
+    if (need > (size_t)WISP_NOALLOC_SCRATCH_BYTES)
+      return fail(WISP_E_WORKSPACE, "the batch needs %zu bytes of scratch, more than the %zu of the static "
+                  "per-device scratch (use wisp_verify with a workspace)", need, (size_t)WISP_NOALLOC_SCRATCH_BYTES);
+    char *ws = nullptr;
+    if ((st = noalloc_scratch(&ws)) != WISP_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    if (!target_logits) target_logits = reinterpret_cast<float *>(ws + p.total);
+    if ((st = upload_by_arguments(p, ws, s)) != WISP_OK) return st;
+    return run_verify(p, model, kv, desc, tokens, draft_probs, rng_seed, accept_len, out_tokens, target_logits,
+                      ws, fault, s);
   });
 }
 

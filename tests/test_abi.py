@@ -203,3 +203,17 @@ def test_gemm_plan_of_the_wide_projections(W):
     assert W.gemm_plan(44, 1024, 256)["kind"] == 1
     with pytest.raises(W.WispError):
         W.gemm_plan(0, 1024, 256)
+
+
+def test_noalloc_rejects_batches_beyond_its_static_scratch(W):
+    """wisp_verify_noalloc refuses a batch whose scratch exceeds WISP_NOALLOC_SCRATCH_BYTES
+    with WISP_E_WORKSPACE, before any GPU work (fake device pointers are never touched)."""
+    L = W.load_library()
+    m = _model(W, n_layers=2, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128, d_ff=14336,
+               vocab=128256, dtype=W.WISP_BF16)
+    big = _desc(W, [2048] * 256, [8] * 256, stride=160)
+    kv = W.wisp_kv(FAKE, FAKE, 100000, 16)
+    st = L.wisp_verify_noalloc(C.byref(m), C.byref(kv), C.byref(big.c), FAKE, FAKE, 1, FAKE, FAKE, FAKE, None, None)
+    assert st == W.WISP_E_WORKSPACE, st
+    assert "static" in W.wisp_last_error()
+    assert W.wisp_workspace_size(m, big) > 128 << 20
