@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwisp.so")
-SOURCES = ["wisp_api.hip", "gemm.hip", "attention.hip", "layers.hip", "sampler.hip", "draft_stats.hip", "scheduler.cpp", "kv_manager.cpp"]
+SOURCES = ["wisp_api.hip", "gemm.hip", "gemm_tile.hip", "attention.hip", "layers.hip", "sampler.hip", "draft_stats.hip", "scheduler.cpp", "kv_manager.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

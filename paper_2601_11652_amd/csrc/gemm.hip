@@ -221,6 +221,23 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
   const int KF = K / 16;
+  // Large row counts are bound by the matrix cores: LDS-staged output tiles, one K range
+  // (measured with cold weights at 343-1237 rows of the 8B and 70B shapes: from 16 row
+  // fragments on the tiles beat the weight ring on every projection, 128 x 256 tiles with
+  // 8 waves for most and 256 x 256 for the LM head; from 10 fragments they win at the 70B
+  // widths, K >= 8192, with 128 x 128 tiles below 16384 columns)
+  if (K % 32 == 0 && (mf >= 16 || (mf >= 10 && K >= 8192))) {
+    c.kind = 4;
+    c.variant = mf >= 16 ? (N >= 65536 ? 3 : 7) : (N >= 16384 ? 7 : 2);
+    const int bm = c.variant == 3 ? 256 : 128, bn = c.variant == 2 ? 128 : 256;
+    c.bm = bm;
+    c.bn = bn;
+    c.mt = bm / 32;
+    c.rb = (mf + c.mt - 1) / c.mt;
+    c.splits = 1;
+    c.kf_per_split = KF;
+    return c;
+  }
   // rows in rb blocks of at most 8 fragments, balanced; each block is one grid row of
   // workgroups that stream the same weights (the grid width is a multiple of 8 for every
   // projection here, so a tile's row blocks share an XCD and its L2)
@@ -274,6 +291,10 @@ static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W,
 
 void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
                const GemmCfg &cfg, hipStream_t s) {
+  if (cfg.kind == 4) {
+    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, s);
+    return;
+  }
   dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, cfg.rb, 1);
   if (cfg.kind == 1)
     launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);

@@ -25,7 +25,9 @@ inline void launch(void (*kernel)(Formals...), dim3 grid, dim3 block, uint32_t s
 // ----- GEMMs: C[z][M][ldc] (fp32) = A[M][K] . W[N][K]^T over the z-th K range ----------
 struct GemmCfg {
   int kind;         // 1: weight ring NT=1 R=8, 2: weight ring NT=2 R=4,
-                    // 3: weight ring NT=1 R=8 with 8 waves (two per SIMD on half the rows each)
+                    // 3: weight ring NT=1 R=8 with 8 waves (two per SIMD on half the rows each),
+                    // 4: LDS-staged output tiles (gemm_bf16_tile, `variant`)
+  int variant;      // kind 4: tile shape (see gemm_bf16_tile)
   int mt;           // 32-row fragments of A held by every workgroup
   int rb;           // row blocks (grid rows): rb * mt fragments cover ceil(M/32)
   int bm, bn;       // tile rows / cols
@@ -36,6 +38,10 @@ GemmCfg gemm_bf16_plan(int M, int N, int K);
 void gemm_bf16(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K,
                int ldc, const GemmCfg &cfg, hipStream_t s);
 void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int ldc, hipStream_t s);
+// large row counts: output tiles of 128 x 128 (variant 2), 128 x 256 with 8 waves (7) or
+// 256 x 256 with one K step per stage (3), both operands staged through LDS
+void gemm_bf16_tile(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K, int ldc,
+                    int variant, hipStream_t s);
 void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hipStream_t s);
 
 // ----- per-row layers --------------------------------------------------------------------

@@ -457,6 +457,7 @@ StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_bloc
 
 int gemm_class(const Plan &p, const GemmCfg &c) {
   if (!p.bf16) return WISP_PROF_GEMM_TILED;
+  if (c.kind == 4) return WISP_PROF_GEMM_TILE;
   return c.kind == 2 ? WISP_PROF_GEMM_RING2 : WISP_PROF_GEMM_RING1;
 }
 

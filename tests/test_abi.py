@@ -191,16 +191,21 @@ def test_binding_rejects_host_and_mistyped_tensors(W):
 
 def test_gemm_plan_of_the_wide_projections(W):
     """The plan picks the 64-column weight ring (variant 2) for outputs of >= 16384
-    columns: gate/up and the LM head of the wide test model (d_model 512, d_ff 8192,
-    vocabulary 32768) in one and in two row blocks, with two K ranges for gate/up; the
-    32-column ring below that width."""
-    for M, rb in ((44, 1), (510, 2)):
+    columns below 16 row fragments: gate/up and the LM head of the wide test model
+    (d_model 512, d_ff 8192, vocabulary 32768) in one and in two row blocks, with two K
+    ranges for gate/up; the 32-column ring below that width; from 16 row fragments the
+    LDS-staged tiles (variant 4, one K range), and from 10 at K >= 8192."""
+    for M, rb in ((44, 1), (476, 2)):
         gu = W.gemm_plan(M, 2 * 8192, 512)
         lm = W.gemm_plan(M, 32768, 512)
         assert gu["kind"] == 2 and lm["kind"] == 2, (gu, lm)
         assert gu["rb"] == rb and lm["rb"] == rb, (gu, lm)
         assert gu["splits"] == 2, gu
     assert W.gemm_plan(44, 1024, 256)["kind"] == 1
+    for M, N, K in ((680, 16384, 512), (1237, 4096, 14336), (1237, 128256, 4096), (370, 10240, 8192)):
+        t = W.gemm_plan(M, N, K)
+        assert t["kind"] == 4 and t["splits"] == 1, (M, N, K, t)
+    assert W.gemm_plan(343, 6144, 4096)["kind"] != 4
     with pytest.raises(W.WispError):
         W.gemm_plan(0, 1024, 256)
 

@@ -8,7 +8,7 @@
 * a batch of plain-decode requests only (no draft rows; the draft distributions may be
   NULL);
 * more than 256 rows (24 requests x 17 rows = 408), which the weight-ring GEMMs serve in
-  two row blocks, and 2108 rows (124 x 17) in nine;
+  two row blocks, and 2108 rows (124 x 17), which run the LDS-staged tile GEMM;
 * 129-256 rows, where the 32-column weight-ring GEMM runs 8 waves on two row halves: an
   odd number of 32-row fragments (150 rows: one half carries a zero fragment) and an even
   one (192 rows);
@@ -16,7 +16,8 @@
   it, and wisp_check reports a device input error;
 * a bf16 model of odd widths: d_model 96, d_ff 160, 3 query heads on 1 kv head, vocabulary
   1056.  Every projection then has a partly filled last column tile and a K shorter than
-  one weight ring, and the GQA group is not a power of two.
+  one weight ring, and the GQA group is not a power of two; at 34 rows (weight ring) and
+  612 rows (tile GEMM).
 """
 import numpy as np
 import pytest
@@ -122,7 +123,7 @@ def test_more_than_256_rows_in_row_blocks():
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs)
 
 
-def test_2108_rows_in_nine_row_blocks():
+def test_2108_rows_in_lds_staged_tiles():
     B = 124
     ctx = [int(c) for c in np.random.default_rng(6).integers(0, 40, size=B)]
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs)
@@ -223,3 +224,13 @@ def test_fault_record_is_sticky_across_calls():
     assert "token id" in str(e.value)
     W.wisp_verify(gm.c, kv, desc, good, q, 5, acc, out, logits, ws)
     W.wisp_check(ws)
+
+
+def test_odd_widths_bf16_at_tile_row_counts():
+    """The odd-width model with 612 rows: every projection runs the LDS-staged tile kernel
+    with partly filled last row and column tiles (1056 = 4 x 256 + 32 columns, 96 = 3 x 32
+    inputs) and a K of 3 to 5 stages."""
+    B = 36
+    ctx = [int(c) for c in np.random.default_rng(7).integers(0, 60, size=B)]
+    _run_case(ODD_BF16, ctx, [16] * B, _bf16_abs)
+
