@@ -33,10 +33,16 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 # timing classes of the library's profiling hook (include/wisp.h) and the kernels they cover
 KERNEL_CLASSES = ((0, "gemm_ring1"), (1, "gemm_ring2"), (2, "gemm_tiled"), (3, "attention"),
-                  (4, "attention_combine"), (5, "rows"), (6, "sampler"))
+                  (4, "attention_combine"), (5, "rows"), (6, "sampler"), (7, "gemm_tile"))
 KERNEL_NAMES = {"gemm_ring1": "gemm_ring_kernel<2, 4, MT/2, 1, 8, 2> (M > 128) / <1, 4, MT, 1, 8, 1>", "gemm_ring2": "gemm_ring_kernel<1, 4, MT, 2, 4, 2>",
                 "gemm_tiled": "gemm_f32_kernel", "attention": "attn_bf16_kernel",
-                "attention_combine": "attn_combine_kernel", "rows": "row kernels", "sampler": "sampler kernels"}
+                "attention_combine": "attn_combine_kernel", "rows": "row kernels", "sampler": "sampler kernels",
+                "gemm_tile": "gemm_tile_kernel (LDS-staged output tiles)"}
+# algorithmic bytes behind every GB/s figure (the library's profiling hook counts these)
+BYTES_DEFINITION = ("GEMM classes: bf16 weights read once (2 N K per projection); attention: the K and V "
+                    "bytes of every cached and new token per kv head; sampler: two fp32 passes over the "
+                    "logits plus one row per request")
+EXTRA_CONFIGS = "8b_b256,8b_dyn128,70b_b64"
 BF16_PEAK_TFLOPS = 2516.6
 FP32_PEAK_TFLOPS = 157.3
 
@@ -94,12 +100,40 @@ def traffic_from_counters(kernel_key: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(mix, order, min_seconds: float = 10.0):
-    """The CPU oracle on a bounded sample of the same workload: requests of the batch in the
-    given order (same weights, context KV, root token and gamma; their drafts come from the
-    oracle's own fixture) until at least min_seconds of oracle time are spent.  Times the
-    oracle's verification of each sampled request, i.e. the forward of its gamma+1 rows
-    plus acceptance; the rate is the sample's committed tokens over that time."""
+def host_info() -> dict:
+    """CPU model, sockets, physical cores and logical CPUs of this host (from /proc/cpuinfo),
+    and the OpenMP thread setting the oracle runs with."""
+    model, phys = None, set()
+    pid = cid = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            k, _, v = line.partition(":")
+            k, v = k.strip(), v.strip()
+            if k == "model name" and model is None:
+                model = v
+            elif k == "physical id":
+                pid = v
+            elif k == "core id":
+                cid = v
+            elif not k and pid is not None:
+                phys.add((pid, cid))
+                pid = cid = None
+        if pid is not None:
+            phys.add((pid, cid))
+    except OSError:
+        pass
+    return {"cpu": model, "sockets": len({p for p, _ in phys}) or None, "physical_cores": len(phys) or None,
+            "logical_cpus": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
+def cpu_baseline(mix, order, inputs, min_seconds: float = 10.0):
+    """The CPU oracle on a bounded sample of the timed batch, on its exact inputs: for the
+    requests in the given order, the same weights, the same context KV (regenerated on the
+    host by the same integer-exact generator, bit for bit), the timed batch's own tokens and
+    draft rows q (copied from the device) and the first timed step's seed, until at least
+    min_seconds of oracle time are spent.  Times the oracle's verification of each sampled
+    request: the forward of its gamma+1 rows plus acceptance; the rate is the sample's
+    committed tokens over that time."""
     import numpy as np
     import oracle
     import wisp_inputs as wi
@@ -108,24 +142,23 @@ def cpu_baseline(mix, order, min_seconds: float = 10.0):
     t0 = time.time()
     model = fx.host_model(s, mix.seed)
     log(f"cpu baseline: host weights generated in {time.time() - t0:.1f} s")
-    roots_all = wi.root_tokens(mix)
+    off = np.concatenate([[0], np.cumsum(mix.rows)])
+    doff = np.concatenate([[0], np.cumsum(mix.gamma)])
     dt = 0.0
     committed = 0
     done = []
     for i in order:
         i = int(i)
         sub = wi.custom_mix(s, [mix.ctx_len[i]], [mix.gamma[i]], seed=mix.seed, name=mix.config)
-        sub.t_draft[:] = mix.t_draft[i]
-        sub.sigma[:] = mix.sigma[i]
         n_pages = (int(mix.ctx_len[i]) + int(mix.gamma[i]) + 1 + 15) // 16
         pt = np.arange(n_pages, dtype=np.int32)[None, :]
         pools = fx.empty_pools(s, n_pages)
         fx.place_synthetic_kv(sub, pools, pt, req_keys=[i])
-        work = (pools[0].copy(), pools[1].copy())
-        toks, qs, _ = fx.draft_fixture(model, sub, work, pt, roots_all[i:i + 1])
+        toks = inputs["tokens"][off[i]:off[i + 1]]
+        q = inputs["q"][doff[i]:doff[i + 1]]
         t1 = time.time()
-        logits = oracle.forward(model, pools[0], pools[1], pt, sub.ctx_len, sub.rows, toks[0])
-        res = oracle.accept(logits, toks[0], qs[0], sub.gamma, 1.0, wi.verify_seed(mix), req_id=[i])
+        logits = oracle.forward(model, pools[0], pools[1], pt, sub.ctx_len, sub.rows, toks)
+        res = oracle.accept(logits, toks, q, sub.gamma, 1.0, inputs["seed"], req_id=mix.req_id[i:i + 1])
         dt += time.time() - t1
         committed += int(res.accept_len[0]) + 1
         done.append(i)
@@ -133,17 +166,20 @@ def cpu_baseline(mix, order, min_seconds: float = 10.0):
             f"{dt:.1f} s of oracle time so far")
         if dt >= min_seconds:
             break
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    host = host_info()
+    threads = int(host["omp_num_threads"] or os.cpu_count() or 1)
     ctx = [int(mix.ctx_len[i]) for i in done]
     gam = [int(mix.gamma[i]) for i in done]
-    return {"value": committed / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": (f"{len(done)} requests of the {mix.config} batch around its median context "
-                       f"(ctx {min(ctx)}-{max(ctx)}, gamma {min(gam)}-{max(gam)}): forward of their "
-                       f"gamma+1 rows through all {s.n_layers} layers plus acceptance, {committed} "
-                       f"committed tokens in {dt:.2f} s of oracle time")}
+    return {"value": committed / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{len(done)} requests of the timed {mix.config} batch around its median context "
+                       f"(ctx {min(ctx)}-{max(ctx)}, gamma {min(gam)}-{max(gam)}) on the timed step's exact "
+                       f"inputs (tokens, draft rows q, context KV, seed): forward of their gamma+1 rows through "
+                       f"all {s.n_layers} layers plus acceptance, {committed} committed tokens in {dt:.2f} s of "
+                       f"oracle time on {threads} OpenMP threads"),
+            "host": host}
 
 
-def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = True):
+def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = True, keep_inputs: bool = False):
     """Fill the KV pool and draft fixture of `mix`, then time `steps` verification steps
     (after `warmup` untimed ones) back to back on the current stream.  Returns the step
     figures and, with `profile`, the per-kernel-class durations."""
@@ -188,6 +224,7 @@ def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = Tr
         ev[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    W.wisp_check(ws)        # device-side input faults of the timed steps
     ms_step = ev[0].elapsed_time(ev[-1]) / steps
     per_step = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(steps)])
     log(f"B = {mix.B}: {steps} steps: {ms_step:.3f} ms/step (events), {wall / steps * 1e3:.3f} ms/step (wall)")
@@ -195,6 +232,8 @@ def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = Tr
     committed = float((L + 1).sum()) / steps
     res = {"ms_per_step": ms_step, "ms_p50": float(np.median(per_step)), "ms_p90": float(np.percentile(per_step, 90)),
            "committed": committed, "accepted": float(L.sum()) / steps, "M": M}
+    if keep_inputs:
+        res["inputs"] = {"tokens": tokens.cpu().numpy(), "q": q.cpu().numpy(), "seed": seed + warmup}
 
     classes = {}
     if profile:
@@ -215,6 +254,7 @@ def measure_workload(W, wi, gm, mix, steps: int, warmup: int, profile: bool = Tr
                                  "achieved_GBs": by.value / ms.value / 1e6 if ms.value else 0.0,
                                  "achieved_TFLOPs": fl.value / ms.value / 1e9 if ms.value else 0.0}
         W.lib.wisp_profile_enable(0)
+        W.wisp_check(ws)
     res["classes"] = classes
     del kv, ws, logits, q
     return res
@@ -233,13 +273,44 @@ def step_lower_bound(classes: dict) -> dict:
     return {"lower_bound_ms": lb * 1e3, "bytes_per_step": by}
 
 
+def class_roofline(name: str, c: dict, M: int) -> dict | None:
+    """One kernel class against its roofline: GEMMs at large row counts (>= 630, twice the
+    MFMA ridge) against the bf16 MFMA peak, everything with algorithmic bytes against the
+    HBM peak; overhead classes (no algorithmic bytes) have none."""
+    if name.startswith("gemm") and M >= 630 and c["flops_per_launch"] > 0:
+        r = {"bound": "mfma", "achieved": c["achieved_TFLOPs"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    elif c["bytes_per_launch"] > 0:
+        r = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        return None
+    r["frac"] = r["achieved"] / r["peak"]
+    return r
+
+
+def config_summary(mix, r) -> dict:
+    """Step time, committed tokens/s, step lower bound and per-class rooflines of one
+    measured workload."""
+    lb = step_lower_bound(r["classes"])
+    classes = {}
+    for name, c in r["classes"].items():
+        classes[name] = {"ms_per_step": c["ms_per_step"], "launches_per_step": c["launches_per_step"],
+                         "avg_launch_us": c["avg_launch_us"], "roofline": class_roofline(name, c, r["M"])}
+    return {"workload": f"{mix.config}: {mix.shape.name} verification step", "B": mix.B, "rows": r["M"],
+            "sum_ctx": int(mix.ctx_len.sum()), "sum_gamma": int(mix.gamma.sum()),
+            "ms_per_step": r["ms_per_step"], "ms_p50": r["ms_p50"], "ms_p90": r["ms_p90"],
+            "committed_tokens_per_step": r["committed"], "tokens_per_s": r["committed"] / (r["ms_per_step"] / 1e3),
+            "step_lower_bound_ms": lb["lower_bound_ms"], "step_frac": lb["lower_bound_ms"] / r["ms_per_step"],
+            "classes": classes}
+
+
 def sweep(args, W, wi, gm):
     """The batch-size curve: the same request distributions at B = 1 .. 256, one JSON line
     per batch size (tokens/s and step latency), written to --sweep-out as well."""
     rows = []
     for B in [int(b) for b in args.sweep.split(",")]:
         mix = wi.make_mix(args.config, B=B)
-        r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True)
+        r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True,
+                         keep_inputs=not args.no_cpu_baseline)
         lb = step_lower_bound(r["classes"])
         row = {"B": B, "rows": r["M"], "sum_ctx": int(mix.ctx_len.sum()), "ms_per_step": r["ms_per_step"],
                "ms_p50": r["ms_p50"], "ms_p90": r["ms_p90"], "committed_tokens_per_step": r["committed"],
@@ -265,6 +336,8 @@ def main():
     ap.add_argument("--sweep", default=None, help="comma-separated batch sizes: print the batch-size curve instead")
     ap.add_argument("--sweep-out", default=None, help="also write the curve to this JSON file")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--configs", default=EXTRA_CONFIGS,
+                    help="further workloads measured after the headline one ('' for none)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM counter scaling)")
     args = ap.parse_args()
@@ -289,7 +362,8 @@ def main():
         sweep(args, W, wi, gm)
         return
 
-    r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True)
+    r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True,
+                         keep_inputs=not args.no_cpu_baseline)
     ms_step = r["ms_per_step"]
     committed = r["committed"]
     value = committed / (ms_step / 1e3)
@@ -304,6 +378,7 @@ def main():
         roof = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["kernel"] = KERNEL_NAMES[dom]
+    roof["bytes_definition"] = BYTES_DEFINITION
     roof["traffic"] = traffic_from_counters(f"{dom}_{args.config}")
     lb = step_lower_bound(classes)
 
@@ -340,6 +415,31 @@ def main():
         "roofline": roof,
         "kernels": classes,
     }
+    for name, c in classes.items():
+        c["roofline"] = class_roofline(name, c, M)
+    # the other workloads of the "vs batch B" curve (step time, tokens/s, lower bound and the
+    # per-class rooflines of each), fewer steps each
+    extra = [c for c in args.configs.split(",") if c and c != args.config]
+    if extra:
+        cfgs = {}
+        inputs = r.pop("inputs", None)
+        cur = s
+        for name in extra:
+            m2 = wi.make_mix(name)
+            if m2.shape != cur:
+                del gm
+                torch.cuda.empty_cache()
+                t0 = time.time()
+                cur = m2.shape
+                gm = W.GpuModel(cur, lambda l: wi.layer_weights(cur, l, m2.seed, "cuda"),
+                                wi.global_weights(cur, m2.seed, "cuda"))
+                log(f"{name}: weights generated and packed in {time.time() - t0:.1f} s")
+            r2 = measure_workload(W, wi, gm, m2, min(args.steps, 8), min(args.warmup, 2), profile=True)
+            cfgs[name] = config_summary(m2, r2)
+            log(f"{name}: {r2['ms_per_step']:.2f} ms/step, {cfgs[name]['tokens_per_s']:.0f} tokens/s")
+            torch.cuda.empty_cache()
+        result["configs"] = cfgs
+        r["inputs"] = inputs
     if not args.no_cpu_baseline:
         # requests outward from the median context: median, next above, next below, ...
         by_ctx = np.argsort(mix.ctx_len, kind="stable")
@@ -347,7 +447,7 @@ def main():
         order = [by_ctx[mid + (k + 1) // 2 * (1 if k % 2 else -1)] for k in range(2 * mix.B)
                  if 0 <= mid + (k + 1) // 2 * (1 if k % 2 else -1) < mix.B]
         try:
-            result["cpu_baseline"] = cpu_baseline(mix, order)
+            result["cpu_baseline"] = cpu_baseline(mix, order, r["inputs"])
         except MemoryError as e:   # report rather than fail the GPU measurement
             result["cpu_baseline"] = {"value": None, "error": str(e)}
     print(json.dumps(result), flush=True)

@@ -247,7 +247,7 @@ wisp_status wisp_check(void *workspace, void *stream);
  * pair of HIP events on the caller's stream that the runtime stamps with the dispatch's own
  * begin and end, and the class accumulates the measured milliseconds, the launch count and
  * the algorithmic bytes / flops of its launches:
- *   GEMM classes: 2-byte (bf16) or 4-byte weights N*K + activations M*K + fp32 result M*N;
+ *   GEMM classes: the weights, 2 (bf16) or 4 (fp32) bytes x N*K, read once per step;
  *   ATTN: K and V bytes of every token each kv head reads (ctx_len + gamma + 1 per request);
  *   SAMPLER: two passes over the fp32 logits plus one row per request;
  *   ATTN_COMBINE, ROWS: none (overhead kernels).

@@ -484,7 +484,9 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
   const int32_t *vrow = reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow;
 
   const double es = p.bf16 ? 2.0 : 4.0;
-  auto gemm_bytes = [&](int N, int K) { return es * ((double)N * K + (double)p.M * K) + 4.0 * p.M * N; };
+  // algorithmic bytes of a projection: its weights, read once per step (activations and
+  // results are a few percent at the step's row counts and not counted)
+  auto gemm_bytes = [&](int N, int K) { return es * (double)N * K; };
   auto gemm_flops = [&](int N, int K) { return 2.0 * p.M * N * K; };
   const double kv_tok = 2.0 * p.nkv * p.hd * es;   // K and V bytes per token per layer
   double attn_bytes = 0.0, attn_flops = 0.0;
@@ -557,7 +559,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
     }
   }
   {
-    const double lm_bytes = es * ((double)p.V * p.d + (double)p.Mv * p.d) + 4.0 * p.Mv * p.V;
+    const double lm_bytes = es * (double)p.V * p.d;
     ProfScope ps(gemm_class(p, p.g_lm), lm_bytes, 2.0 * p.Mv * p.V * p.d, s);
     if (p.bf16)
       gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.Mv, p.V, p.d, p.V, p.g_lm, s);

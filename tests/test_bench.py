@@ -26,3 +26,16 @@ def test_step_lower_bound_takes_the_longer_roof_per_class():
     lb = bench.step_lower_bound(classes)
     assert lb["bytes_per_step"] == pytest.approx(8e9 + 1e6)
     assert lb["lower_bound_ms"] == pytest.approx(8e9 / (bench.HBM_PEAK_GBS * 1e9) * 1e3 + 2000.0)
+
+
+def test_host_description_and_class_rooflines():
+    sys.path.insert(0, ROOT)
+    import bench
+    h = bench.host_info()
+    assert set(h) == {"cpu", "sockets", "physical_cores", "logical_cpus", "omp_num_threads"}
+    assert h["logical_cpus"] >= 1
+    gemm = {"bytes_per_launch": 1e8, "flops_per_launch": 1e12, "achieved_GBs": 4000.0, "achieved_TFLOPs": 1258.3}
+    assert bench.class_roofline("gemm_tile", gemm, 1237)["bound"] == "mfma"
+    assert bench.class_roofline("gemm_tile", gemm, 1237)["frac"] == pytest.approx(0.5)
+    assert bench.class_roofline("gemm_ring1", gemm, 171)["bound"] == "hbm"
+    assert bench.class_roofline("rows", {"bytes_per_launch": 0, "flops_per_launch": 0}, 171) is None
