@@ -16,7 +16,11 @@ Prints ONE JSON line.  Also reports the median and p90 step time, the whole step
 its roofline lower bound (each kernel class's algorithmic bytes or flops at the HBM or
 MFMA peak), the dominant kernel class against its roofline (algorithmic bytes per launch
 over the HIP-event-timed average launch) and the CPU oracle timed on a bounded sample of
-the same workload.  `--sweep 1,2,4,...` prints the batch-size curve instead.
+the same batch, on its exact inputs.  The same line carries the other workloads of the
+curve (`configs`: 8b_b256, 8b_dyn128, 70b_b64 by default) with their step times, rates,
+lower bounds and per-class rooflines.  The parent process touches no GPU: each workload
+is measured by a child process of its own (`--worker`), which is also the form to run
+under a profiler.  `--sweep 1,2,4,...` prints the batch-size curve instead.
 """
 from __future__ import annotations
 
@@ -326,6 +330,77 @@ def sweep(args, W, wi, gm):
                        "command": command_line(None)}, f, indent=1)
 
 
+def worker(args) -> None:
+    """GPU side: one workload measured in this process; prints its record as one JSON line
+    (and, with --dump-inputs, writes the timed batch's inputs for the CPU baseline)."""
+    import numpy as np
+    import torch
+    import paper_2601_11652_amd as W
+    import wisp_inputs as wi
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    mix = wi.make_mix(args.config, B=args.B)
+    s = mix.shape
+    t0 = time.time()
+    gm = W.GpuModel(s, lambda l: wi.layer_weights(s, l, mix.seed, "cuda"), wi.global_weights(s, mix.seed, "cuda"))
+    log(f"{args.config}: weights generated and packed in {time.time() - t0:.1f} s")
+    if args.sweep:
+        sweep(args, W, wi, gm)
+        return
+
+    r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True, keep_inputs=bool(args.dump_inputs))
+    if args.dump_inputs:
+        inp = r.pop("inputs")
+        np.savez(args.dump_inputs, tokens=inp["tokens"], q=inp["q"], seed=np.uint64(inp["seed"]))
+    ms_step = r["ms_per_step"]
+    committed = r["committed"]
+    classes = r["classes"]
+    M = mix.M
+    dom = max((k for k in classes if classes[k]["bytes_per_launch"] > 0), key=lambda k: classes[k]["ms_per_step"])
+    c = classes[dom]
+    if dom.startswith("gemm") and M >= 630:
+        roof = {"bound": "mfma", "achieved": c["achieved_TFLOPs"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["kernel"] = KERNEL_NAMES[dom]
+    roof["traffic"] = traffic_from_counters(f"{dom}_{args.config}")
+    roof["bytes_definition"] = BYTES_DEFINITION
+    for name, cl in classes.items():
+        cl["roofline"] = class_roofline(name, cl, M)
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log("copy calibration: 1 GiB device-to-device copy done")
+    rec = config_summary(mix, r)
+    rec.update({"dtype": "bf16" if s.dtype == "bf16" else "f32", "layers": s.n_layers, "vocab": s.vocab,
+                "accepted_drafts_per_s": r["accepted"] / (ms_step / 1e3),
+                "acceptance_rate": r["accepted"] / max(1, int(mix.gamma.sum())),
+                "roofline": roof, "kernels": classes})
+    print(json.dumps(rec), flush=True)
+
+
+def run_worker(args, config: str, steps: int, warmup: int, dump: str | None = None) -> dict:
+    """One workload in a child process of its own: device memory a process frees is not
+    handed back for its own reuse on this stack, so each workload starts from a whole GPU."""
+    import subprocess
+    cmd = [sys.executable, os.path.abspath(__file__), "--worker", "--config", config, "--steps", str(steps),
+           "--warmup", str(warmup)]
+    if args.B is not None and config == args.config:
+        cmd += ["--B", str(args.B)]
+    if dump:
+        cmd += ["--dump-inputs", dump]
+    if args.copy_calibration and config == args.config:
+        cmd += ["--copy-calibration"]
+    p = subprocess.run(cmd, stdout=subprocess.PIPE, text=True)
+    if p.returncode != 0:
+        raise SystemExit(f"bench worker for {config} failed with status {p.returncode}")
+    return json.loads(p.stdout.strip().splitlines()[-1])
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -340,116 +415,73 @@ def main():
                     help="further workloads measured after the headline one ('' for none)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM counter scaling)")
+    ap.add_argument("--worker", action="store_true",
+                    help="measure --config in this process and print its record (what the parent runs)")
+    ap.add_argument("--dump-inputs", default=None, help=argparse.SUPPRESS)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one MI355X only; --gpus {args.gpus} is not supported (requests are "
               "independent, so N GPUs run N replicas; see the design notes)", file=sys.stderr)
         sys.exit(2)
-
-    import numpy as np
-    import torch
-    import paper_2601_11652_amd as W
-    import wisp_inputs as wi
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    mix = wi.make_mix(args.config, B=args.B)
-    s = mix.shape
-    t0 = time.time()
-    gm = W.GpuModel(s, lambda l: wi.layer_weights(s, l, mix.seed, "cuda"), wi.global_weights(s, mix.seed, "cuda"))
-    log(f"weights generated and packed in {time.time() - t0:.1f} s")
-    if args.sweep:
-        sweep(args, W, wi, gm)
+    if args.worker or args.sweep:
+        worker(args)
         return
 
-    r = measure_workload(W, wi, gm, mix, args.steps, args.warmup, profile=True,
-                         keep_inputs=not args.no_cpu_baseline)
-    ms_step = r["ms_per_step"]
-    committed = r["committed"]
-    value = committed / (ms_step / 1e3)
-    classes = r["classes"]
-    M = mix.M
-    dom = max((k for k in classes if classes[k]["bytes_per_launch"] > 0), key=lambda k: classes[k]["ms_per_step"])
-    c = classes[dom]
-    mfma_bound = dom.startswith("gemm") and M >= 630
-    if mfma_bound:
-        roof = {"bound": "mfma", "achieved": c["achieved_TFLOPs"], "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": c["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["kernel"] = KERNEL_NAMES[dom]
-    roof["bytes_definition"] = BYTES_DEFINITION
-    roof["traffic"] = traffic_from_counters(f"{dom}_{args.config}")
-    lb = step_lower_bound(classes)
-
-    if args.copy_calibration:
-        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        b = torch.empty_like(a)
-        b.copy_(a)
-        torch.cuda.synchronize()
-        log("copy calibration: 1 GiB device-to-device copy done")
-
+    # parent: touches no GPU itself; each workload runs in a child process
+    import tempfile
+    import numpy as np
+    import wisp_inputs as wi
+    tmp = tempfile.mkdtemp(prefix="wisp_bench_")
+    dump = None if args.no_cpu_baseline else os.path.join(tmp, "inputs.npz")
+    h = run_worker(args, args.config, args.steps, args.warmup, dump)
+    mix = wi.make_mix(args.config, B=args.B)
     result = {
         "metric": "accepted tokens/s + verify-step latency (ms) vs batch B, 8B-shape bf16",
-        "value": value,
+        "value": h["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
+        "ms_per_step": h["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if s.dtype == "bf16" else "f32",
+        "dtype": h["dtype"],
         "data": "synthetic (seeded random-init weights, synthetic paged context KV, drafts from the target's own logits plus noise)",
-        "config": {"workload": f"{args.config}: {s.name} verification step", "B": mix.B, "rows": M,
-                   "sum_ctx": int(mix.ctx_len.sum()), "sum_gamma": int(mix.gamma.sum()), "page": 16,
-                   "layers": s.n_layers, "vocab": s.vocab},
-        "ms_p50": r["ms_p50"],
-        "ms_p90": r["ms_p90"],
-        "accepted_drafts_per_s": r["accepted"] / (ms_step / 1e3),
-        "acceptance_rate": r["accepted"] / max(1, int(mix.gamma.sum())),
-        "committed_tokens_per_step": committed,
-        "step_roofline": {"lower_bound_ms": lb["lower_bound_ms"], "frac": lb["lower_bound_ms"] / ms_step,
-                          "bytes_per_step": lb["bytes_per_step"]},
-        "roofline": roof,
-        "kernels": classes,
+        "config": {"workload": h["workload"], "B": h["B"], "rows": h["rows"], "sum_ctx": h["sum_ctx"],
+                   "sum_gamma": h["sum_gamma"], "page": 16, "layers": h["layers"], "vocab": h["vocab"]},
+        "ms_p50": h["ms_p50"],
+        "ms_p90": h["ms_p90"],
+        "accepted_drafts_per_s": h["accepted_drafts_per_s"],
+        "acceptance_rate": h["acceptance_rate"],
+        "committed_tokens_per_step": h["committed_tokens_per_step"],
+        "step_roofline": {"lower_bound_ms": h["step_lower_bound_ms"], "frac": h["step_frac"]},
+        "roofline": h["roofline"],
+        "kernels": h["kernels"],
     }
-    for name, c in classes.items():
-        c["roofline"] = class_roofline(name, c, M)
-    # the other workloads of the "vs batch B" curve (step time, tokens/s, lower bound and the
-    # per-class rooflines of each), fewer steps each
+    # the other workloads of the "vs batch B" curve: step time, tokens/s, lower bound and the
+    # per-class rooflines of each (fewer steps each)
     extra = [c for c in args.configs.split(",") if c and c != args.config]
     if extra:
-        cfgs = {}
-        inputs = r.pop("inputs", None)
-        cur = s
+        result["configs"] = {}
         for name in extra:
-            m2 = wi.make_mix(name)
-            if m2.shape != cur:
-                del gm
-                torch.cuda.empty_cache()
-                t0 = time.time()
-                cur = m2.shape
-                gm = W.GpuModel(cur, lambda l: wi.layer_weights(cur, l, m2.seed, "cuda"),
-                                wi.global_weights(cur, m2.seed, "cuda"))
-                log(f"{name}: weights generated and packed in {time.time() - t0:.1f} s")
-            r2 = measure_workload(W, wi, gm, m2, min(args.steps, 8), min(args.warmup, 2), profile=True)
-            cfgs[name] = config_summary(m2, r2)
-            log(f"{name}: {r2['ms_per_step']:.2f} ms/step, {cfgs[name]['tokens_per_s']:.0f} tokens/s")
-            torch.cuda.empty_cache()
-        result["configs"] = cfgs
-        r["inputs"] = inputs
-    if not args.no_cpu_baseline:
+            result["configs"][name] = run_worker(args, name, min(args.steps, 8), min(args.warmup, 2))
+            log(f"{name}: {result['configs'][name]['ms_per_step']:.2f} ms/step, "
+                f"{result['configs'][name]['tokens_per_s']:.0f} tokens/s")
+    if dump:
         # requests outward from the median context: median, next above, next below, ...
         by_ctx = np.argsort(mix.ctx_len, kind="stable")
         mid = mix.B // 2
         order = [by_ctx[mid + (k + 1) // 2 * (1 if k % 2 else -1)] for k in range(2 * mix.B)
                  if 0 <= mid + (k + 1) // 2 * (1 if k % 2 else -1) < mix.B]
+        z = np.load(dump)
+        inputs = {"tokens": z["tokens"], "q": z["q"], "seed": int(z["seed"])}
         try:
-            result["cpu_baseline"] = cpu_baseline(mix, order, r["inputs"])
+            result["cpu_baseline"] = cpu_baseline(mix, order, inputs)
         except MemoryError as e:   # report rather than fail the GPU measurement
             result["cpu_baseline"] = {"value": None, "error": str(e)}
+        os.remove(dump)
+    os.rmdir(tmp)
     print(json.dumps(result), flush=True)
 
 
