@@ -225,8 +225,9 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   // (measured with cold weights at 343-1237 rows of the 8B and 70B shapes: from 16 row
   // fragments on the tiles beat the weight ring on every projection, 128 x 256 tiles with
   // 8 waves for most and 256 x 256 for the LM head; from 10 fragments they win at the 70B
-  // widths, K >= 8192, with 128 x 128 tiles below 16384 columns)
-  if (K % 32 == 0 && (mf >= 16 || (mf >= 10 && K >= 8192))) {
+  // widths, N and K >= 8192, with 128 x 128 tiles below 16384 columns; at the 8B widths
+  // the ring stays faster there)
+  if (K % 32 == 0 && (mf >= 16 || (mf >= 10 && K >= 8192 && N >= 8192))) {
     c.kind = 4;
     c.variant = mf >= 16 ? (N >= 65536 ? 3 : 7) : (N >= 16384 ? 7 : 2);
     const int bm = c.variant == 3 ? 256 : 128, bn = c.variant == 2 ? 128 : 256;

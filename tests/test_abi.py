@@ -194,7 +194,7 @@ def test_gemm_plan_of_the_wide_projections(W):
     columns below 16 row fragments: gate/up and the LM head of the wide test model
     (d_model 512, d_ff 8192, vocabulary 32768) in one and in two row blocks, with two K
     ranges for gate/up; the 32-column ring below that width; from 16 row fragments the
-    LDS-staged tiles (variant 4, one K range), and from 10 at K >= 8192."""
+    LDS-staged tiles (variant 4, one K range), and from 10 at the 70B widths (N, K >= 8192)."""
     for M, rb in ((44, 1), (476, 2)):
         gu = W.gemm_plan(M, 2 * 8192, 512)
         lm = W.gemm_plan(M, 32768, 512)
@@ -205,7 +205,7 @@ def test_gemm_plan_of_the_wide_projections(W):
     for M, N, K in ((680, 16384, 512), (1237, 4096, 14336), (1237, 128256, 4096), (370, 10240, 8192)):
         t = W.gemm_plan(M, N, K)
         assert t["kind"] == 4 and t["splits"] == 1, (M, N, K, t)
-    assert W.gemm_plan(343, 6144, 4096)["kind"] != 4
+    assert W.gemm_plan(343, 6144, 4096)["kind"] != 4 and W.gemm_plan(343, 4096, 14336)["kind"] != 4
     with pytest.raises(W.WispError):
         W.gemm_plan(0, 1024, 256)
 
