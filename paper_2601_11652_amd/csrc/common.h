@@ -149,6 +149,78 @@ constexpr uint32_t kTagAccept = 1u;
 constexpr uint32_t kTagRace = 2u;
 
 // ---------------------------------------------------------------------------------------
+// Optional output of a single-K-range projection (the LM head): per row and output tile of
+// the GEMM's tile width in columns, the row's maximum over the tile and the first column
+// holding it, m[row * tiles + tile]; m == NULL: not computed.
+// ---------------------------------------------------------------------------------------
+struct RowMaxOut {
+  float *m;
+  int32_t *i;
+  int tiles;
+};
+
+// Each row's maximum over one output tile's columns, and the first column holding it, from
+// the fp32 accumulators just stored (the LM head's logits).  Lane l of a wave holds column
+// l % 32 of each of its fragments for rows 4 (l / 32) + 8 (e / 4) + e % 4; a row's values
+// are reduced over the wave's fragments, then over the 32 lanes of its half-wave
+// (butterfly), then over the WGN waves of the tile's column range through LDS, in column
+// order.  Ties keep the smaller column.  `sh` holds WGN x (WGM * MTW * 32) values and as
+// many columns.
+template <int WGM, int WGN, int MTW, int NTW>
+__device__ __forceinline__ void tile_row_max(const floatx16 (&acc)[MTW][NTW], float *sh, int nb_first, int NF, int N,
+                                             int M, int row0, int wrf, int wn, int tile, RowMaxOut rm) {
+  constexpr int ROWS = WGM * MTW * 32;
+  const int lane = threadIdx.x & 63;
+  int *shc = reinterpret_cast<int *>(sh + WGN * ROWS);
+#pragma unroll
+  for (int i = 0; i < MTW; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      float bv = -INFINITY;
+      int bc = 0x7FFFFFFF;
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const int col = (nb_first + j) * 32 + (lane & 31);
+        if (nb_first + j < NF && col < N && acc[i][j][e] > bv) {
+          bv = acc[i][j][e];
+          bc = col;
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) {
+        const float ov = __shfl_xor(bv, o);
+        const int oc = __shfl_xor(bc, o);
+        if (ov > bv || (ov == bv && oc < bc)) {
+          bv = ov;
+          bc = oc;
+        }
+      }
+      if ((lane & 31) == 0) {
+        const int lr = (wrf + i) * 32 + 4 * (lane >> 5) + 8 * (e >> 2) + (e & 3);
+        sh[wn * ROWS + lr] = bv;
+        shc[wn * ROWS + lr] = bc;
+      }
+    }
+  __syncthreads();
+  for (int lr = threadIdx.x; lr < ROWS; lr += blockDim.x) {
+    const int row = row0 + lr;
+    if (row >= M) continue;
+    float bv = sh[lr];
+    int bc = shc[lr];
+    for (int w = 1; w < WGN; ++w) {
+      const float ov = sh[w * ROWS + lr];
+      const int oc = shc[w * ROWS + lr];
+      if (ov > bv || (ov == bv && oc < bc)) {
+        bv = ov;
+        bc = oc;
+      }
+    }
+    rm.m[(int64_t)row * rm.tiles + tile] = bv;
+    rm.i[(int64_t)row * rm.tiles + tile] = bc;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
 // error word bits (kept in the first bytes of the workspace)
 // ---------------------------------------------------------------------------------------
 constexpr int kErrToken = 1;

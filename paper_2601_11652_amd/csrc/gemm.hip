@@ -30,7 +30,7 @@ template <int WM, int WN, int MT, int NT, int R, int AD>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t *__restrict__ A,
                                                            const uint16_t *__restrict__ W,
                                                            float *__restrict__ C, int M, int N, int K,
-                                                           int ldc, int kf_per_split) {
+                                                           int ldc, int kf_per_split, RowMaxOut rmax) {
   constexpr int BMF = WM * MT;
   constexpr int NTH = 64 * WM * WN;             // threads per workgroup
   constexpr int A_FR = BMF * R;                 // A fragments per chunk
@@ -202,6 +202,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_ring_kernel(const uint16_t 
       }
     }
   }
+  if (rmax.m) {   // LM head (one K range): the row maxima of this tile's columns
+    __syncthreads();   // the activation buffers are free now
+    tile_row_max<WM, WN, MT, NT>(acc, reinterpret_cast<float *>(&lds[0][0][0]), nbw, NF, N, M,
+                                 rb0 * 32, wm * MT, wn, tile, rmax);
+  }
 }
 
 static constexpr int kNarrowAD = 1;   // activation prefetch depth of the 32-column ring
@@ -265,19 +270,19 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
 
 // 32-column ring, 8 waves: two row halves of ceil(mt / 2) fragments each
 static void launch_ring_paired(int mt, dim3 grid, const uint16_t *A, const uint16_t *W, float *C, int M,
-                               int N, int K, int ldc, int kps, hipStream_t s) {
+                               int N, int K, int ldc, int kps, RowMaxOut rm, hipStream_t s) {
   switch ((mt + 1) / 2) {
-    case 3: launch(gemm_ring_kernel<2, 4, 3, 1, 8, 2>, grid, 512, 0, s, A, W, C, M, N, K, ldc, kps); break;
-    case 4: launch(gemm_ring_kernel<2, 4, 4, 1, 8, 2>, grid, 512, 0, s, A, W, C, M, N, K, ldc, kps); break;
+    case 3: launch(gemm_ring_kernel<2, 4, 3, 1, 8, 2>, grid, 512, 0, s, A, W, C, M, N, K, ldc, kps, rm); break;
+    case 4: launch(gemm_ring_kernel<2, 4, 4, 1, 8, 2>, grid, 512, 0, s, A, W, C, M, N, K, ldc, kps, rm); break;
   }
 }
 
 template <int NT, int R, int AD>
 static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W, float *C, int M,
-                        int N, int K, int ldc, int kps, hipStream_t s) {
+                        int N, int K, int ldc, int kps, RowMaxOut rm, hipStream_t s) {
   switch (mt) {
 #define WISP_RING_CASE(X) \
-  case X: launch(gemm_ring_kernel<1, 4, X, NT, R, AD>, grid, 256, 0, s, A, W, C, M, N, K, ldc, kps); break;
+  case X: launch(gemm_ring_kernel<1, 4, X, NT, R, AD>, grid, 256, 0, s, A, W, C, M, N, K, ldc, kps, rm); break;
     WISP_RING_CASE(1)
     WISP_RING_CASE(2)
     WISP_RING_CASE(3)
@@ -291,18 +296,18 @@ static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W,
 }
 
 void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
-               const GemmCfg &cfg, hipStream_t s) {
+               const GemmCfg &cfg, hipStream_t s, RowMaxOut rm) {
   if (cfg.kind == 4) {
-    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, s);
+    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, rm, s);
     return;
   }
   dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, cfg.rb, 1);
   if (cfg.kind == 1)
-    launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+    launch_ring<1, 8, kNarrowAD>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, rm, s);
   else if (cfg.kind == 3)
-    launch_ring_paired(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+    launch_ring_paired(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, rm, s);
   else
-    launch_ring<2, 4, 2>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, s);
+    launch_ring<2, 4, 2>(cfg.mt, grid, A, W, C, M, N, K, ldc, cfg.kf_per_split, rm, s);
 }
 
 // ---------------------------------------------------------------------------------------

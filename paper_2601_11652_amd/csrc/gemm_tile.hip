@@ -49,7 +49,8 @@ template <int WGM, int WGN, int MTW, int NTW, int KS, int ST>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_t *__restrict__ A,
                                                         const uint16_t *__restrict__ W,
                                                         float *__restrict__ C, int M, int N, int K,
-                                                        int ldc, int tiles_m, int tiles, int per_xcd) {
+                                                        int ldc, int tiles_m, int tiles, int per_xcd,
+                                                        RowMaxOut rmax) {
   constexpr int NW = WGM * WGN;               // waves
   constexpr int AF = WGM * MTW, BF = WGN * NTW;   // A / W fragments of the tile per K step
   constexpr int SF = (AF + BF) * KS;          // fragments per stage
@@ -178,24 +179,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
       }
     }
   }
+  if (rmax.m) {   // LM head: the row maxima of this tile's columns
+    __syncthreads();   // every wave is done with the stage buffers (no load is in flight)
+    tile_row_max<WGM, WGN, MTW, NTW>(acc, reinterpret_cast<float *>(&lds0[0][0]), nb0 + wn * NTW, NF, N, M,
+                                     rb0 * 32, wm * MTW, wn, tn, rmax);
+  }
 }
 
 template <int WGM, int WGN, int MTW, int NTW, int KS, int ST>
 static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
-                        hipStream_t s) {
+                        RowMaxOut rm, hipStream_t s) {
+  static_assert(2 * WGN * WGM * MTW * 32 * 4 <= (WGM * MTW + WGN * NTW) * KS * 1024,
+                "the row-maxima exchange fits one stage buffer");
   const int tiles_m = ((M + 31) / 32 + WGM * MTW - 1) / (WGM * MTW);
   const int tiles_n = (N / 32 + WGN * NTW - 1) / (WGN * NTW);
   const int tiles = tiles_m * tiles_n, per_xcd = (tiles + 7) / 8;
   launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K, ldc,
-         tiles_m, tiles, per_xcd);
+         tiles_m, tiles, per_xcd, rm);
 }
 
 void gemm_bf16_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc, int variant,
-                    hipStream_t s) {
+                    RowMaxOut rm, hipStream_t s) {
   switch (variant) {
-    case 2: launch_tile<2, 2, 2, 2, 2, 6>(A, W, C, M, N, K, ldc, s); break;   // 128 x 128, 4 waves
-    case 3: launch_tile<2, 2, 4, 4, 1, 6>(A, W, C, M, N, K, ldc, s); break;   // 256 x 256, 4 waves
-    case 7: launch_tile<2, 4, 2, 2, 2, 5>(A, W, C, M, N, K, ldc, s); break;   // 128 x 256, 8 waves
+    case 2: launch_tile<2, 2, 2, 2, 2, 6>(A, W, C, M, N, K, ldc, rm, s); break;   // 128 x 128, 4 waves
+    case 3: launch_tile<2, 2, 4, 4, 1, 6>(A, W, C, M, N, K, ldc, rm, s); break;   // 256 x 256, 4 waves
+    case 7: launch_tile<2, 4, 2, 2, 2, 5>(A, W, C, M, N, K, ldc, rm, s); break;   // 128 x 256, 8 waves
   }
 }
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "common.h"
+
 namespace wisp {
 
 // ----- kernel launch ---------------------------------------------------------------------
@@ -36,12 +38,12 @@ struct GemmCfg {
 };
 GemmCfg gemm_bf16_plan(int M, int N, int K);
 void gemm_bf16(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K,
-               int ldc, const GemmCfg &cfg, hipStream_t s);
+               int ldc, const GemmCfg &cfg, hipStream_t s, RowMaxOut rm = RowMaxOut{nullptr, nullptr, 0});
 void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int ldc, hipStream_t s);
 // large row counts: output tiles of 128 x 128 (variant 2), 128 x 256 with 8 waves (7) or
 // 256 x 256 with one K step per stage (3), both operands staged through LDS
 void gemm_bf16_tile(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K, int ldc,
-                    int variant, hipStream_t s);
+                    int variant, RowMaxOut rm, hipStream_t s);
 void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hipStream_t s);
 
 // ----- per-row layers --------------------------------------------------------------------
@@ -114,9 +116,10 @@ struct SamplerScratch {   // carved from the workspace; sizes from sampler_chunk
   int32_t *req_R;         // [B] first rejection
 };
 int sampler_chunks(int V);
+// lm: the LM head's per-tile row maxima of these logits (RowMaxOut), or m == NULL
 void sampler(const StepDesc &d, int B, int M, int V, const float *logits, const int32_t *tokens,
              const float *q, float T, uint64_t seed, SamplerScratch sc, int32_t *accept_len,
-             int32_t *out_tokens, hipStream_t s);
+             int32_t *out_tokens, hipStream_t s, RowMaxOut lm = RowMaxOut{nullptr, nullptr, 0});
 void uniform_draws(uint64_t seed, uint32_t req, uint32_t tag, uint32_t row, uint32_t n, float *out,
                    hipStream_t s);
 void clear_ints(int *p, int n, hipStream_t s);

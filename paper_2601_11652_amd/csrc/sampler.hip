@@ -3,8 +3,10 @@
 // token -- drawn from norm(max(0, p_R - q_R)) after a rejection (the residual that makes
 // speculative sampling lossless) and from p after a fully accepted block.
 //
-// Four launches per batch, each over vocabulary chunks of 8192 entries: the row maxima of
-// z = logits / T (argmax at T = 0), the fp64 sums of exp(z - max), then one workgroup per
+// Four launches per batch, over vocabulary chunks of 8192 entries: the row maxima of
+// z = logits / T (argmax at T = 0) -- from the LM head's per-tile maxima when the step's own
+// GEMM produced them, so the logits are read in full only once more --, the fp64 sums of
+// exp(z - max), then one workgroup per
 // (request, chunk) decides every draft in parallel (thread j - 1 takes draft j; R is the
 // smallest rejected j, an integer minimum) and runs its chunk of the exponential race that
 // samples the extra token (argmax of score - ln(-ln u): no prefix sums, so the result does
@@ -92,6 +94,35 @@ __global__ __launch_bounds__(256) void row_max_kernel(const float *__restrict__ 
   block_argmax(bk, bi, shk, shi);
   if (threadIdx.x == 0) {
     part_m[r * CH + c] = bk;
+    part_i[r * CH + c] = bi;
+  }
+}
+
+// pass 1 from the LM head's tile maxima (max and first argmax of the raw logits over each
+// output tile): the same values as a pass over the logits.  z = l / T is monotone in l for
+// T > 0, so max z = (max l) / T exactly, and the first argmax of l is that of z.  The row's
+// result fills all CH chunk slots, so the later passes read it unchanged.
+__global__ __launch_bounds__(256) void row_max_from_tiles_kernel(const float *__restrict__ tile_m,
+                                                                 const int32_t *__restrict__ tile_i, int tiles,
+                                                                 float T, int CH, float *__restrict__ part_m,
+                                                                 int32_t *__restrict__ part_i) {
+  __shared__ float shk[4];
+  __shared__ int shi[4];
+  const int64_t r = blockIdx.x;
+  float bk = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int t = threadIdx.x; t < tiles; t += 256) {
+    const float v = tile_m[r * tiles + t];
+    const int c = tile_i[r * tiles + t];
+    if (better(v, c, bk, bi)) {
+      bk = v;
+      bi = c;
+    }
+  }
+  block_argmax(bk, bi, shk, shi);
+  const float m = T == 0.f ? bk : bk / T;
+  for (int c = threadIdx.x; c < CH; c += 256) {
+    part_m[r * CH + c] = m;
     part_i[r * CH + c] = bi;
   }
 }
@@ -281,10 +312,14 @@ int sampler_chunks(int V) { return (V + kVChunk - 1) / kVChunk; }
 
 void sampler(const StepDesc &d, int B, int M, int V, const float *logits, const int32_t *tokens,
              const float *q, float T, uint64_t seed, SamplerScratch sc, int32_t *accept_len,
-             int32_t *out_tokens, hipStream_t s) {
+             int32_t *out_tokens, hipStream_t s, RowMaxOut lm) {
   if (B == 0) return;
   const int CH = sampler_chunks(V);
-  launch(row_max_kernel, dim3(M, CH), 256, 0, s, logits, V, T, CH, sc.part_m, sc.part_i);
+  if (lm.m)
+    launch(row_max_from_tiles_kernel, M, 256, 0, s, (const float *)lm.m, (const int32_t *)lm.i, lm.tiles, T, CH,
+           sc.part_m, sc.part_i);
+  else
+    launch(row_max_kernel, dim3(M, CH), 256, 0, s, logits, V, T, CH, sc.part_m, sc.part_i);
   if (T != 0.f) launch(row_sum_kernel, dim3(M, CH), 256, 0, s, logits, V, T, CH, sc.part_m, sc.part_s);
   launch(race_kernel, dim3(B, CH), 256, 0, s, d, V, logits, tokens, q, T, seed, CH, sc.part_m, sc.part_i,
                                           sc.part_s, sc.race_k, sc.race_i, sc.req_R);

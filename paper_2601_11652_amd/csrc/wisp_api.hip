@@ -55,7 +55,8 @@ struct Plan {
   // byte offsets inside the workspace
   size_t w_err = 0, w_desc = 0, w_rope = 0, w_h = 0, w_xn = 0, w_ao = 0, w_af = 0, w_q = 0,
          w_part = 0, w_attn_o = 0, w_attn_ml = 0, w_sm = 0, w_si = 0, w_ss = 0, w_rk = 0, w_ri = 0,
-         w_rR = 0, w_vtok = 0, total = 0;
+         w_rR = 0, w_vtok = 0, w_lmm = 0, w_lmi = 0, total = 0;
+  int lm_tiles = 0;                  // output tiles of the LM head (bf16): its row-maxima columns
 };
 
 
@@ -305,6 +306,11 @@ wisp_status make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bo
     carve(w, p.w_part, part * p.M * 4);
     carve(w, p.w_attn_o, p.items.size() * (size_t)p.hd * 64 * 4);
     carve(w, p.w_attn_ml, p.items.size() * 64 * 2 * 4);
+    if (p.bf16) {
+      p.lm_tiles = (p.V + p.g_lm.bn - 1) / p.g_lm.bn;
+      carve(w, p.w_lmm, (size_t)p.Mv * p.lm_tiles * 4);
+      carve(w, p.w_lmi, (size_t)p.Mv * p.lm_tiles * 4);
+    }
   }
   p.total = w;
   return WISP_OK;
@@ -455,6 +461,12 @@ StepDesc step_desc(const Plan &p, char *ws, const wisp_batch_desc *d, int n_bloc
   return sd;
 }
 
+// the LM head's per-tile row maxima (bf16 path), which spare the sampler a pass over the logits
+RowMaxOut lm_row_max(const Plan &p, char *ws) {
+  if (!p.bf16 || p.lm_tiles == 0) return RowMaxOut{nullptr, nullptr, 0};
+  return RowMaxOut{reinterpret_cast<float *>(ws + p.w_lmm), reinterpret_cast<int32_t *>(ws + p.w_lmi), p.lm_tiles};
+}
+
 int gemm_class(const Plan &p, const GemmCfg &c) {
   if (!p.bf16) return WISP_PROF_GEMM_TILED;
   if (c.kind == 4) return WISP_PROF_GEMM_TILE;
@@ -562,7 +574,8 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
     const double lm_bytes = es * (double)p.V * p.d;
     ProfScope ps(gemm_class(p, p.g_lm), lm_bytes, 2.0 * p.Mv * p.V * p.d, s);
     if (p.bf16)
-      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.Mv, p.V, p.d, p.V, p.g_lm, s);
+      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->lm_head, logits, p.Mv, p.V, p.d, p.V, p.g_lm, s,
+                lm_row_max(p, ws));
     else
       gemm_f32((const float *)xn, (const float *)m->lm_head, logits, p.Mv, p.V, p.d, p.V, s);
   }
@@ -617,9 +630,12 @@ wisp_status run_verify(const Plan &p, const wisp_model *model, const wisp_kv *kv
     gather_ints(tokens, reinterpret_cast<const int32_t *>(ws + p.w_desc) + p.i_vrow, p.Mv, g, s);
     vtok = g;
   }
-  ProfScope ps(WISP_PROF_SAMPLER, 2.0 * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
+  // algorithmic bytes: one fp32 pass over the logits (the maxima come with the LM head in
+  // bf16; the fp32 path makes two passes) plus one logits row and one q row per request
+  const RowMaxOut lm = lm_row_max(p, ws);
+  ProfScope ps(WISP_PROF_SAMPLER, (lm.m ? 1.0 : 2.0) * p.Mv * p.V * 4.0 + 2.0 * p.B * p.V * 4.0, 0, s);
   sampler(sv, p.B, p.Mv, p.V, target_logits, vtok, draft_probs, desc->temperature, rng_seed,
-          sampler_scratch(p, ws), accept_len, out_tokens, s);
+          sampler_scratch(p, ws), accept_len, out_tokens, s, lm);
   return hip_check("sampler launch");
 }
 
