@@ -262,7 +262,7 @@ wisp_status wisp_check(void *workspace, void *stream);
 #define WISP_PROF_ATTN_COMBINE 4 /* attn_combine_kernel                                  */
 #define WISP_PROF_ROWS 5         /* embedding, norms, RoPE + KV append, SwiGLU           */
 #define WISP_PROF_SAMPLER 6      /* acceptance kernels                                    */
-#define WISP_PROF_GEMM_TILE 7    /* gemm_tile_kernel, LDS-staged output tiles (large row counts) */
+#define WISP_PROF_GEMM_TILE 7    /* gemm_tile_kernel, LDS-staged output tiles (>= 161 rows) */
 #define WISP_PROF_KINDS 8
 wisp_status wisp_profile_enable(int on);
 wisp_status wisp_profile_read(int kind, double *ms, int64_t *launches, double *bytes, double *flops);
@@ -272,7 +272,7 @@ wisp_status wisp_profile_reset(void);
  * Launch plan of one bf16 projection of the step (host only; introspection for tests and
  * benchmarks): M rows, N output columns, K inputs.  out[0] = kernel variant (1: 32-column
  * weight ring, 2: 64-column weight ring, 3: 32-column weight ring with two waves per SIMD,
- * 4: LDS-staged output tiles for large row counts), out[1] = row blocks (row tiles),
+ * 4: LDS-staged output tiles, from 161 rows), out[1] = row blocks (row tiles),
  * out[2] = 32-row fragments per row block, out[3] = K ranges whose fp32 partial sums are
  * added in fixed order.  WISP_E_INVALID for M, N or K < 1, or N and
  * K not multiples of 32 and 16.

@@ -226,23 +226,31 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
   const int KF = K / 16;
-  // Large row counts are bound by the matrix cores: LDS-staged output tiles, one K range
-  // (measured with cold weights at 343-1237 rows of the 8B and 70B shapes: from 16 row
-  // fragments on the tiles beat the weight ring on every projection, 128 x 256 tiles with
-  // 8 waves for most and 256 x 256 for the LM head; from 10 fragments they win at the 70B
-  // widths, N and K >= 8192, with 128 x 128 tiles below 16384 columns; at the 8B widths
-  // the ring stays faster there)
-  if (K % 32 == 0 && (mf >= 16 || (mf >= 10 && K >= 8192 && N >= 8192))) {
-    c.kind = 4;
-    c.variant = mf >= 16 ? (N >= 65536 ? 3 : 7) : (N >= 16384 ? 7 : 2);
-    const int bm = c.variant == 3 ? 256 : 128, bn = c.variant == 2 ? 128 : 256;
-    c.bm = bm;
-    c.bn = bn;
-    c.mt = bm / 32;
-    c.rb = (mf + c.mt - 1) / c.mt;
-    c.splits = 1;
-    c.kf_per_split = KF;
-    return c;
+  // From 6 row fragments on, LDS-staged output tiles (measured with cold weights at
+  // 171-1237 rows of the 8B and 70B projections: faster than the weight ring on every
+  // projection but the 8B output projection at 171 rows, where the two are level).  One
+  // row tile where the rows fit 192, 256 or 384 rows, 256-row tiles beyond; K split in
+  // powers of two while the work items fit one round of 256 workgroups and each split
+  // keeps at least 8 chunks.  Below 6 fragments the weight ring keeps fewer idle rows.
+  {
+    const int variant = mf <= 6 ? (N >= 16384 ? 4 : 1) : mf <= 8 ? 13 : mf <= 12 ? 12 : 13;
+    const TileShape ts = tile_shape(variant);
+    if (mf >= 6 && K % (16 * ts.ks) == 0) {
+      const int tiles = ((mf * 32 + ts.bm - 1) / ts.bm) * ((N + ts.bn - 1) / ts.bn);
+      const int KC = K / (16 * ts.ks);
+      int s = 1;
+      while (s < 8 && tiles * s * 2 <= 256 && KC / (s * 2) >= 8) s *= 2;
+      const int kcs = (KC + s - 1) / s;
+      c.kind = 4;
+      c.variant = variant;
+      c.bm = ts.bm;
+      c.bn = ts.bn;
+      c.mt = ts.bm / 32;
+      c.rb = (mf * 32 + ts.bm - 1) / ts.bm;
+      c.splits = (KC + kcs - 1) / kcs;
+      c.kf_per_split = kcs * ts.ks;
+      return c;
+    }
   }
   // rows in rb blocks of at most 8 fragments, balanced; each block is one grid row of
   // workgroups that stream the same weights (the grid width is a multiple of 8 for every
@@ -298,7 +306,7 @@ static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W,
 void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
                const GemmCfg &cfg, hipStream_t s, RowMaxOut rm) {
   if (cfg.kind == 4) {
-    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, rm, s);
+    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, cfg.kf_per_split / tile_shape(cfg.variant).ks, rm, s);
     return;
   }
   dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, cfg.rb, 1);

@@ -36,6 +36,13 @@ __device__ __forceinline__ void lds_dma16(const void *src, const void *dst) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void *)dst);
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(m0) : "memory", "m0");
 }
+// the same for data read once (the weight stream): marked non-temporal, so the caches do
+// not keep it at the expense of the activation slices that the other tiles re-read (measured
+// on weight-heavy tiles: the weight stream runs about a third faster)
+__device__ __forceinline__ void lds_dma16_stream(const void *src, const void *dst) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void *)dst);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" : : "v"(src), "s"(m0) : "memory", "m0");
+}
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding: vmcnt in bits
 // 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima)
@@ -50,7 +57,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
                                                         const uint16_t *__restrict__ W,
                                                         float *__restrict__ C, int M, int N, int K,
                                                         int ldc, int tiles_m, int tiles, int per_xcd,
-                                                        RowMaxOut rmax) {
+                                                        int kc_split, RowMaxOut rmax) {
   constexpr int NW = WGM * WGN;               // waves
   constexpr int AF = WGM * MTW, BF = WGN * NTW;   // A / W fragments of the tile per K step
   constexpr int SF = (AF + BF) * KS;          // fragments per stage
@@ -80,14 +87,22 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
   const int KF = K >> 4, MF = (M + 31) >> 5, NF = N >> 5;
-  const int KC = KF / KS;                     // K chunks (K is a multiple of 16 KS)
+  const int KC_all = KF / KS;                 // K chunks (K is a multiple of 16 KS)
   // Workgroups are dealt to the 8 XCDs in turn (id mod 8).  Each XCD takes a contiguous run
   // of per_xcd tiles, column-tile major, so the workgroups resident on one XCD share the
   // A row slices and W column slices of few tiles, which its L2 then serves; the mapping
   // only moves traffic between cache levels, results do not depend on it.
+  // Work items are (K range, tile) pairs, K range major: an XCD's run mostly shares one K
+  // range, i.e. one slice of A, in its L2.  K range z sums chunks [z kc_split, ...) into
+  // its own fp32 partial C[z]; the consumer adds the partials in fixed order.
   const int v = (int)(blockIdx.x % 8u) * per_xcd + (int)(blockIdx.x / 8u);
-  if (v >= tiles) return;
-  const int tm = v % tiles_m, tn = v / tiles_m;
+  const int splits = (KC_all + kc_split - 1) / kc_split;
+  if (v >= tiles * splits) return;
+  const int z = v / tiles, t = v % tiles;
+  const int tm = t % tiles_m, tn = t / tiles_m;
+  const int kc0 = z * kc_split;
+  const int KC = min(KC_all, kc0 + kc_split) - kc0;
+  C += (int64_t)z * M * ldc;
   const int rb0 = tm * AF, nb0 = tn * BF;
 
   // this wave's loads of chunk c into stage buffer b: fragment f of the stage is A block
@@ -98,16 +113,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
 #pragma unroll
     for (int t = 0; t < LPW; ++t) {
       const int f = wave * LPW + t;
-      const uint16_t *src;
       if (f < AF * KS) {
-        const int rb = min(rb0 + f / KS, MF - 1), kb = c * KS + f % KS;
-        src = A + ((int64_t)rb * KF + kb) * 512;
+        const int rb = min(rb0 + f / KS, MF - 1), kb = (kc0 + c) * KS + f % KS;
+        lds_dma16(A + ((int64_t)rb * KF + kb) * 512 + lane * 8, &buf[f][0]);
       } else {
         const int g = f - AF * KS;
-        const int nb = min(nb0 + g / KS, NF - 1), kb = c * KS + g % KS;
-        src = W + ((int64_t)nb * KF + kb) * 512;
+        const int nb = min(nb0 + g / KS, NF - 1), kb = (kc0 + c) * KS + g % KS;
+        lds_dma16_stream(W + ((int64_t)nb * KF + kb) * 512 + lane * 8, &buf[f][0]);
       }
-      lds_dma16(src + lane * 8, &buf[f][0]);
     }
   };
 
@@ -119,28 +132,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  static_for<ST - 1>([&](auto sb) {
-    if (sb.value < KC) issue(sb.value, sb);
-  });
-
-  // one step of the ring: chunk c sits in stage buffer B; the load of chunk c + ST - 1 goes
-  // to buffer (B + ST - 1) % ST, freed by chunk c - 1
-  auto step = [&](int c, auto bc) {
-    constexpr int B = decltype(bc)::value;
-    // chunk c's loads (this wave's) have landed once at most the later in-flight chunks'
-    // remain; at the tail fewer chunks are in flight, so wait for all
-    if (c + ST - 2 < KC)
-      wait_vmcnt<(ST - 2) * LPW>();
-    else
-      wait_vmcnt<0>();
-    // every wave's loads of chunk c are in LDS, and every wave is done reading chunk c - 1
-    // (its reads completed before its last products): a bare barrier, no memory fence
-    __builtin_amdgcn_s_barrier();
-    if (c + ST - 1 < KC) issue(c + ST - 1, std::integral_constant<int, (B + ST - 1) % ST>{});
-    uint4 (*buf)[64] = stage(bc);
-    // all of the stage's operands are read up front, so the reads of step k + 1 overlap the
-    // products of step k
-    uint4 a[KS][MTW], w[KS][NTW];
+  // this wave's operands of the chunk in stage buffer b, read from LDS into registers
+  auto read_ops = [&](auto b, uint4 (&a)[KS][MTW], uint4 (&w)[KS][NTW]) {
+    uint4 (*buf)[64] = stage(b);
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
 #pragma unroll
@@ -148,6 +142,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
 #pragma unroll
       for (int j = 0; j < NTW; ++j) w[k][j] = buf[AF * KS + (wn * NTW + j) * KS + k][lane];
     }
+  };
+  auto products = [&](const uint4 (&a)[KS][MTW], const uint4 (&w)[KS][NTW]) {
 #pragma unroll
     for (int k = 0; k < KS; ++k)
 #pragma unroll
@@ -157,11 +153,39 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[k][i]), as_bf16x8(w[k][j]), acc[i][j],
                                                              0, 0, 0);
   };
-  int c = 0;
-  for (; c + ST <= KC; c += ST) static_for<ST>([&](auto bc) { step(c + bc.value, bc); });
-  static_for<ST>([&](auto bc) {
-    if (c + bc.value < KC) step(c + bc.value, bc);
+
+  static_for<ST - 1>([&](auto sb) {
+    if (sb.value < KC) issue(sb.value, sb);
   });
+  // one step of the ring: chunk c sits in stage buffer B; the load of chunk c + ST - 1 goes
+  // to buffer (B + ST - 1) % ST, freed by chunk c - 1.  With `guarded` false the caller
+  // knows c + ST - 1 < KC (steady state), so the step has no conditions: with them the
+  // compiler keeps the accumulators of the two paths in different registers and copies
+  auto step = [&](int c, auto bc, auto guarded) {
+    constexpr int B = decltype(bc)::value;
+    constexpr bool G = decltype(guarded)::value;
+    // chunk c's loads (this wave's) have landed once at most the later in-flight chunks'
+    // remain; at the tail fewer chunks are in flight, so wait for all
+    if (!G || c + ST - 2 < KC)
+      wait_vmcnt<(ST - 2) * LPW>();
+    else
+      wait_vmcnt<0>();
+    // every wave's loads of chunk c are in LDS, and every wave is done reading chunk c - 1
+    // (its reads completed before its last products): a bare barrier, no memory fence
+    __builtin_amdgcn_s_barrier();
+    if (!G || c + ST - 1 < KC) issue(c + ST - 1, std::integral_constant<int, (B + ST - 1) % ST>{});
+    // all of the stage's operands are read up front, so the reads of step k + 1 overlap the
+    // products of step k
+    uint4 a[KS][MTW], w[KS][NTW];
+    read_ops(bc, a, w);
+    products(a, w);
+  };
+  int c = 0;
+  for (; c + 2 * ST - 2 < KC; c += ST) static_for<ST>([&](auto bc) { step(c + bc.value, bc, std::false_type{}); });
+  for (; c < KC; c += ST)
+    static_for<ST>([&](auto bc) {
+      if (c + bc.value < KC) step(c + bc.value, bc, std::true_type{});
+    });
 
   wait_vmcnt<0>();
 #pragma unroll
@@ -188,22 +212,38 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
 
 template <int WGM, int WGN, int MTW, int NTW, int KS, int ST>
 static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
-                        RowMaxOut rm, hipStream_t s) {
+                        RowMaxOut rm, hipStream_t s, int kc_split) {
   static_assert(2 * WGN * WGM * MTW * 32 * 4 <= (WGM * MTW + WGN * NTW) * KS * 1024,
                 "the row-maxima exchange fits one stage buffer");
   const int tiles_m = ((M + 31) / 32 + WGM * MTW - 1) / (WGM * MTW);
   const int tiles_n = (N / 32 + WGN * NTW - 1) / (WGN * NTW);
-  const int tiles = tiles_m * tiles_n, per_xcd = (tiles + 7) / 8;
+  const int KC = K / (16 * KS);
+  const int splits = (KC + kc_split - 1) / kc_split;
+  const int tiles = tiles_m * tiles_n, per_xcd = (tiles * splits + 7) / 8;
   launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K, ldc,
-         tiles_m, tiles, per_xcd, rm);
+         tiles_m, tiles, per_xcd, kc_split, rm);
+}
+
+// Tile shapes (measured at 171-1237 rows of the 8B and 70B projections, cold weights):
+// 8 waves in 2 x 4 or 4 x 2 wave tiles of 3 x 1, 3 x 2 or 2 x 2 fragments, two waves per
+// SIMD; the wider the column tile, the fewer times the activation slice is re-read.
+TileShape tile_shape(int variant) {
+  switch (variant) {
+    case 1: return {192, 128, 4};
+    case 4: return {192, 256, 4};
+    case 12: return {384, 128, 2};
+    case 13: return {256, 128, 2};
+  }
+  return {0, 0, 0};
 }
 
 void gemm_bf16_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc, int variant,
-                    RowMaxOut rm, hipStream_t s) {
+                    int kc_split, RowMaxOut rm, hipStream_t s) {
   switch (variant) {
-    case 2: launch_tile<2, 2, 2, 2, 2, 6>(A, W, C, M, N, K, ldc, rm, s); break;   // 128 x 128, 4 waves
-    case 3: launch_tile<2, 2, 4, 4, 1, 6>(A, W, C, M, N, K, ldc, rm, s); break;   // 256 x 256, 4 waves
-    case 7: launch_tile<2, 4, 2, 2, 2, 5>(A, W, C, M, N, K, ldc, rm, s); break;   // 128 x 256, 8 waves
+    case 1: launch_tile<2, 4, 3, 1, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
+    case 4: launch_tile<2, 4, 3, 2, 4, 2>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
+    case 12: launch_tile<4, 2, 3, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
+    case 13: launch_tile<4, 2, 2, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
   }
 }
 

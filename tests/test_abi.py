@@ -190,22 +190,29 @@ def test_binding_rejects_host_and_mistyped_tensors(W):
 
 
 def test_gemm_plan_of_the_wide_projections(W):
-    """The plan picks the 64-column weight ring (variant 2) for outputs of >= 16384
-    columns below 16 row fragments: gate/up and the LM head of the wide test model
-    (d_model 512, d_ff 8192, vocabulary 32768) in one and in two row blocks, with two K
-    ranges for gate/up; the 32-column ring below that width; from 16 row fragments the
-    LDS-staged tiles (variant 4, one K range), and from 10 at the 70B widths (N, K >= 8192)."""
-    for M, rb in ((44, 1), (476, 2)):
-        gu = W.gemm_plan(M, 2 * 8192, 512)
-        lm = W.gemm_plan(M, 32768, 512)
-        assert gu["kind"] == 2 and lm["kind"] == 2, (gu, lm)
-        assert gu["rb"] == rb and lm["rb"] == rb, (gu, lm)
-        assert gu["splits"] == 2, gu
+    """Below 6 row fragments the weight ring: 64-column wave tiles (variant 2) for outputs of
+    >= 16384 columns (gate/up and the LM head of the wide test model, d_model 512, d_ff
+    8192, vocabulary 32768), with two K ranges for gate/up, and 32-column tiles below that
+    width.  From 6 fragments the LDS-staged tiles (variant 4) with K split in powers of two
+    while the work items fit one round of 256 workgroups and each split keeps >= 8 chunks:
+    the 8B projections at 171 rows, the 8B / 70B ones at 343 / 370 rows in one 384-row tile,
+    and 1237 rows in 256-row tiles."""
+    gu = W.gemm_plan(44, 2 * 8192, 512)
+    lm = W.gemm_plan(44, 32768, 512)
+    assert gu["kind"] == 2 and lm["kind"] == 2 and gu["rb"] == 1 and lm["rb"] == 1, (gu, lm)
+    assert gu["splits"] == 2, gu
     assert W.gemm_plan(44, 1024, 256)["kind"] == 1
-    for M, N, K in ((680, 16384, 512), (1237, 4096, 14336), (1237, 128256, 4096), (370, 10240, 8192)):
+    cases = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
+        (171, 6144, 4096): (1, 6, 4), (171, 4096, 4096): (1, 6, 8), (171, 28672, 4096): (1, 6, 2),
+        (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),
+        (343, 6144, 4096): (1, 12, 4), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),
+        (370, 10240, 8192): (1, 12, 2), (370, 8192, 28672): (1, 12, 4),
+        (476, 16384, 512): (2, 8, 1), (680, 16384, 512): (3, 8, 1),
+        (1237, 4096, 14336): (5, 8, 1), (1237, 128256, 4096): (5, 8, 1),
+    }
+    for (M, N, K), (rb, mt, splits) in cases.items():
         t = W.gemm_plan(M, N, K)
-        assert t["kind"] == 4 and t["splits"] == 1, (M, N, K, t)
-    assert W.gemm_plan(343, 6144, 4096)["kind"] != 4 and W.gemm_plan(343, 4096, 14336)["kind"] != 4
+        assert t["kind"] == 4 and (t["rb"], t["mt"], t["splits"]) == (rb, mt, splits), (M, N, K, t)
     with pytest.raises(W.WispError):
         W.gemm_plan(0, 1024, 256)
 
