@@ -229,11 +229,15 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   // From 6 row fragments on, LDS-staged output tiles (measured with cold weights at
   // 171-1237 rows of the 8B and 70B projections: faster than the weight ring on every
   // projection but the 8B output projection at 171 rows, where the two are level).  One
-  // row tile where the rows fit 192, 256 or 384 rows, 256-row tiles beyond; K split in
-  // powers of two while the work items fit one round of 256 workgroups and each split
-  // keeps at least 8 chunks.  Below 6 fragments the weight ring keeps fewer idle rows.
+  // row tile where the rows fit 192, 256 or 384 rows, 256-row tiles beyond, 256 columns
+  // wide only for the LM head at 192 rows (measured over whole steps: for gate/up the
+  // 128-column tile in one K range costs the same and halves the partial sums that the
+  // SwiGLU kernel reads); K split in powers of two while the work items fit one round of
+  // 256 workgroups and each split keeps at least 8 chunks (fewer splits cost the GEMMs
+  // more than the row kernels save).  Below 6 fragments the weight ring keeps fewer idle
+  // rows.
   {
-    const int variant = mf <= 6 ? (N >= 16384 ? 4 : 1) : mf <= 8 ? 13 : mf <= 12 ? 12 : 13;
+    const int variant = mf <= 6 ? (N >= 65536 ? 4 : 1) : mf <= 8 ? 13 : mf <= 12 ? 12 : 13;
     const TileShape ts = tile_shape(variant);
     if (mf >= 6 && K % (16 * ts.ks) == 0) {
       const int tiles = ((mf * 32 + ts.bm - 1) / ts.bm) * ((N + ts.bn - 1) / ts.bn);
