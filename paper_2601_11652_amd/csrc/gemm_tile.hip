@@ -52,7 +52,7 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int WGM, int WGN, int MTW, int NTW, int KS, int ST>
+template <int WGM, int WGN, int MTW, int NTW, int KS, int ST, bool RM>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_t *__restrict__ A,
                                                         const uint16_t *__restrict__ W,
                                                         float *__restrict__ C, int M, int N, int K,
@@ -203,7 +203,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
       }
     }
   }
-  if (rmax.m) {   // LM head: the row maxima of this tile's columns
+  if (RM) {   // LM head: the row maxima of this tile's columns (its own instance: the
+             // maxima need registers that the plain projections spend on their tiles)
     __syncthreads();   // every wave is done with the stage buffers (no load is in flight)
     tile_row_max<WGM, WGN, MTW, NTW>(acc, reinterpret_cast<float *>(&lds0[0][0]), nb0 + wn * NTW, NF, N, M,
                                      rb0 * 32, wm * MTW, wn, tn, rmax);
@@ -220,8 +221,12 @@ static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, i
   const int KC = K / (16 * KS);
   const int splits = (KC + kc_split - 1) / kc_split;
   const int tiles = tiles_m * tiles_n, per_xcd = (tiles * splits + 7) / 8;
-  launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K, ldc,
-         tiles_m, tiles, per_xcd, kc_split, rm);
+  if (rm.m)
+    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, true>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K,
+           ldc, tiles_m, tiles, per_xcd, kc_split, rm);
+  else
+    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, false>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K,
+           ldc, tiles_m, tiles, per_xcd, kc_split, rm);
 }
 
 // Tile shapes (measured at 171-1237 rows of the 8B and 70B projections, cold weights):
