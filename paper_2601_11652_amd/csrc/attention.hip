@@ -320,7 +320,7 @@ void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_gr
                             const float *part_o, const float *part_ml, uint16_t *out, bool out_packed,
                             int out_K, int nq, int nkv, int hd, hipStream_t s) {
   if (n_groups == 0) return;
-  constexpr int kMaxC = 8;
+  constexpr int kMaxC = kAttnCombineChunks;
   if (hd == 128) {
     const int64_t threads = (int64_t)n_groups * kAttnRowsPerItem * 16;
     launch(attn_combine_kernel<128, kMaxC>, (unsigned)((threads + 255) / 256), 256, 0, s,

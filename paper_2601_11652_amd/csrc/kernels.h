@@ -98,6 +98,7 @@ constexpr int kAttnRowsPerItem = 48;   // query rows one wave carries (3 blocks 
 constexpr int kAttnMaxItems = 1 << 22;  // split-KV work items of one call (int indices, workspace)
 constexpr int kAcceptRowsMax = 1 << 29; // rows of one acceptance-only call (int offsets)
 constexpr int kAttnMaxChunkPages = 64; // pages of one item (one block id per lane)
+constexpr int kAttnCombineChunks = 8;  // chunks the combine loads per round of dependent loads
 
 // split-KV partials of every item, then their fixed-order combine into `out`
 void attention_bf16_main(const StepDesc &d, const AttnItem *items, int n_items, const uint16_t *q,

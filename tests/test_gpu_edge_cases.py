@@ -117,7 +117,8 @@ def test_plain_decode_batch_without_draft_rows(shape, check):
             assert abs(ref.race_key1[i] - ref.race_key2[i]) < 1e-3 + 4 * gap, (i, o[i], ref.out_tokens[i])
 
 
-def test_more_than_256_rows_in_row_blocks():
+def test_more_than_256_rows_in_two_row_tiles():
+    """408 rows: two 256-row tiles of the LDS-staged GEMM, the second one mostly padding."""
     B = 24
     ctx = [int(c) for c in np.random.default_rng(5).integers(0, 96, size=B)]
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs)
@@ -129,10 +130,22 @@ def test_2108_rows_in_lds_staged_tiles():
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs)
 
 
-@pytest.mark.parametrize("B,gamma", [(10, 14), (12, 15)], ids=["150rows", "192rows"])
-def test_paired_wave_ring_gemm_rows(B, gamma):
+@pytest.mark.parametrize("B,gamma", [(10, 14), (12, 15)], ids=["150rows-ring", "192rows-tile"])
+def test_rows_around_the_ring_to_tile_switch(B, gamma):
+    """150 rows (5 fragments): the weight ring with two waves per SIMD on half the rows each;
+    192 rows (6 fragments): the 192-row LDS-staged tile with its K split."""
     ctx = [int(c) for c in np.random.default_rng(B).integers(0, 80, size=B)]
     _run_case(MINI_BF16, ctx, [gamma] * B, _bf16_abs)
+
+
+def test_odd_widths_bf16_at_192_rows():
+    """The odd-width model at 192 rows: the projections whose K is an odd multiple of 32
+    (QKV, gate/up and the LM head over d_model 96, down over d_ff 160) keep the paired-wave
+    weight ring at 6 fragments; the output projection (K = 192) runs the 192-row tile on a
+    partly filled column tile."""
+    B = 12
+    ctx = [int(c) for c in np.random.default_rng(8).integers(0, 60, size=B)]
+    _run_case(ODD_BF16, ctx, [15] * B, _bf16_abs)
 
 
 def test_out_of_range_block_id_is_reported():

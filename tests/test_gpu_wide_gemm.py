@@ -1,15 +1,15 @@
 """The wide-output projections at the stated bf16 bound.
 
-gate/up and the LM head run the 64-column weight-ring GEMM once their output is at least
-16384 columns wide, which the 8B / 70B shapes always are and the small test models never
-were.  This model makes both wide at a width the oracle recomputes in seconds: d_model
+Below 6 row fragments gate/up and the LM head run the 64-column weight-ring GEMM once
+their output is at least 16384 columns wide, which the 8B / 70B shapes always are and the
+small test models never were.  This model makes both wide at a width the oracle recomputes in seconds: d_model
 512, 8 query heads on 2 kv heads of 64, d_ff 8192 (gate/up 16384 columns), vocabulary
 32768, bf16, 2 layers.  At d_model 512 the gate/up projection is also split over K (two
 ranges summed in fixed order), the LM head is not.
 
-Cases: 44 rows (one row block of the weight-ring GEMMs), 476 rows (two row blocks of at
-most 256, each re-streaming the weights) and 680 rows (from 16 row fragments on, every
-projection runs the LDS-staged tile kernel instead).  Checks: logits within 2e-2 max-abs of the oracle, every
+Cases: 44 rows (the weight-ring GEMMs, gate/up and the LM head on 64-column wave tiles),
+476 and 680 rows (every projection on the LDS-staged 256-row tiles, in two and three row
+tiles).  Checks: logits within 2e-2 max-abs of the oracle, every
 written K/V value within max(two bf16 ulps at its head vector's scale, twice the oracle's floor of its
 layer), untouched slots bit-identical, decisions on the GPU's own logits bit-exact except
 flagged near-ties.
