@@ -229,15 +229,18 @@ static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, i
            ldc, tiles_m, tiles, per_xcd, kc_split, rm);
 }
 
-// Tile shapes (measured at 171-1237 rows of the 8B and 70B projections, cold weights):
+// Tile shapes (measured at 7-1237 rows of the 8B and 70B projections, cold weights):
 // 8 waves in 2 x 4 or 4 x 2 wave tiles of 3 x 1, 3 x 2 or 2 x 2 fragments, two waves per
-// SIMD; the wider the column tile, the fewer times the activation slice is re-read.
+// SIMD; the wider the column tile, the fewer times the activation slice is re-read.  For
+// at most 32 rows a 32 x 256 tile of 4 waves with a deep K split: its activation slice
+// and fp32 partials are small next to the weights, so the loads are almost all weights.
 TileShape tile_shape(int variant) {
   switch (variant) {
     case 1: return {192, 128, 4};
     case 4: return {192, 256, 4};
     case 12: return {384, 128, 2};
     case 13: return {256, 128, 2};
+    case 5: return {32, 256, 4};
   }
   return {0, 0, 0};
 }
@@ -249,6 +252,7 @@ void gemm_bf16_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N
     case 4: launch_tile<2, 4, 3, 2, 4, 2>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
     case 12: launch_tile<4, 2, 3, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
     case 13: launch_tile<4, 2, 2, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
+    case 5: launch_tile<1, 4, 1, 2, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;   // 4 waves
   }
 }
 

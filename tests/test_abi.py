@@ -202,6 +202,14 @@ def test_gemm_plan_of_the_wide_projections(W):
     assert gu["kind"] == 2 and lm["kind"] == 2 and gu["rb"] == 1 and lm["rb"] == 1, (gu, lm)
     assert gu["splits"] == 2, gu
     assert W.gemm_plan(44, 1024, 256)["kind"] == 1
+    # at most 32 rows: the 32 x 256 tile (up to 16 K ranges) for >= 20M weights below the
+    # LM head's width; the output projection and the LM head stay on the ring
+    for M in (7, 32):
+        assert (W.gemm_plan(M, 6144, 4096)["kind"], W.gemm_plan(M, 6144, 4096)["splits"]) == (4, 8)
+        assert (W.gemm_plan(M, 28672, 4096)["kind"], W.gemm_plan(M, 28672, 4096)["splits"]) == (4, 2)
+        assert (W.gemm_plan(M, 4096, 14336)["kind"], W.gemm_plan(M, 4096, 14336)["splits"]) == (4, 16)
+        assert W.gemm_plan(M, 4096, 4096)["kind"] == 1 and W.gemm_plan(M, 128256, 4096)["kind"] == 2
+    assert W.gemm_plan(33, 6144, 4096)["kind"] == 1
     cases = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
         (171, 6144, 4096): (1, 6, 4), (171, 4096, 4096): (1, 6, 8), (171, 28672, 4096): (1, 6, 1),
         (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),

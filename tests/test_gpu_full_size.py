@@ -24,6 +24,9 @@ the observed logit gap cannot flip them (acceptance margin widened by exp(2 gap)
 margin by 4 gap, residual resample exempt).  Every request: finite logits, an accepted
 prefix equal to the drafts, one valid extra token, -1 padding, no error flag.
 
+The 8b_b32 request mix is also run at B = 3 (at most 27 rows: the QKV, gate/up and down
+projections then take the 32-row GEMM tile with deep K splits, the others the weight ring).
+
 Sampled requests (drafts from the oracle's own autoregressive fixture): the first, a
 plain-decode request where the mix has one, the longest context and the largest gamma;
 the other requests take model-independent seeded drafts.
@@ -87,9 +90,11 @@ def _gather_pages(pool: torch.Tensor, blocks: np.ndarray) -> np.ndarray:
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("config,n_samples", [("8b_b32", 4), ("8b_b256", 3), ("8b_dyn128", 4), ("70b_b64", 2)])
-def test_full_size_verify(config, n_samples):
-    mix = wi.make_mix(config)
+@pytest.mark.parametrize("config,n_samples,B", [("8b_b32", 4, None), ("8b_b32", 3, 3), ("8b_b256", 3, None),
+                                                ("8b_dyn128", 4, None), ("70b_b64", 2, None)],
+                         ids=["8b_b32", "8b_b32-B3", "8b_b256", "8b_dyn128", "70b_b64"])
+def test_full_size_verify(config, n_samples, B):
+    mix = wi.make_mix(config, B=B)
     s = mix.shape
     samples = _samples(mix, n_samples)
     log(f"{config}: B={mix.B} M={mix.M} ctx [{mix.ctx_len.min()}, {mix.ctx_len.max()}] "
