@@ -215,39 +215,43 @@ static constexpr int kNarrowAD = 1;   // activation prefetch depth of the 32-col
 // memory; below it the extra zero rows and doubled weight requests cost more than that buys
 static constexpr int kPairedWavesMinMT = 5;
 
-// Launch plan.  Weight-ring kernels whose workgroups hold all rows of a row block of at most
-// 256 rows (one block for the verification step's sum(gamma+1) rows at moderate batch
-// sizes; more blocks for larger batches and prompt rows, each re-streaming the weights,
-// mostly from L2 / MALL while the blocks of a tile run together); wide outputs use 64-column
-// wave tiles (one A fragment feeds two products), narrow ones 32-column tiles with a deeper
-// ring (8 waves per workgroup from kPairedWavesMinMT row fragments on).  K is split until
-// one workgroup per CU is in flight (one round).
+// Launch plan.  LDS-staged output tiles (gemm_tile.hip) for most shapes, the weight ring
+// (above) where it streams faster or K does not fit the tile's chunk.  Tile variant by
+// row fragments, measured with cold weights on the 8B and 70B projections at 7-1237 rows:
+//   1 (<= 32 rows): the 32 x 256 tile with up to 16 K splits for projections of >= 20M
+//     weights (at 7 rows QKV 13.4 -> 11.5 us, gate/up 44.0 -> 39.4, down 24.0 -> 20.1, LM
+//     head 169.5 -> 158.9); the output projection streams as fast on the ring;
+//   2: 64 x 128 tiles, 3-4: 128 x 128 (10-23 % faster than the ring on QKV, O, gate/up
+//     and down); the LM head stays on the ring;
+//   5: the 192-row tile below 16384 columns (QKV 22.1 -> 19.5 us, down 38.4 -> 32.4); the
+//     ring for gate/up and the LM head;
+//   6: 192-row tiles, 256 columns wide only for the LM head (measured over whole steps: for
+//     gate/up the 128-column tile in one K range costs the same and halves the partial sums
+//     the SwiGLU kernel reads);
+//   7-8: one 256-row tile, 9-12: one 384-row tile, beyond: 256-row tiles.
+// K is split in powers of two while the work items fit one round of 256 workgroups and
+// each split keeps at least 8 chunks (fewer splits cost the GEMMs more than the row
+// kernels save).  The ring holds all rows of a row block of at most 256 rows: 64-column
+// wave tiles for wide outputs, 32-column tiles with a deeper ring otherwise (8 waves per
+// workgroup from kPairedWavesMinMT row fragments on); K split for one resident round.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
   const int KF = K / 16;
-  // From 6 row fragments on, LDS-staged output tiles (measured with cold weights at
-  // 171-1237 rows of the 8B and 70B projections: faster than the weight ring on every
-  // projection but the 8B output projection at 171 rows, where the two are level).  One
-  // row tile where the rows fit 192, 256 or 384 rows, 256-row tiles beyond, 256 columns
-  // wide only for the LM head at 192 rows (measured over whole steps: for gate/up the
-  // 128-column tile in one K range costs the same and halves the partial sums that the
-  // SwiGLU kernel reads); K split in powers of two while the work items fit one round of
-  // 256 workgroups and each split keeps at least 8 chunks (fewer splits cost the GEMMs
-  // more than the row kernels save).  Below 6 fragments the weight ring keeps fewer idle
-  // rows.
-  // At one row fragment (<= 32 rows) the 32 x 256 tile with up to 16 K splits, for the
-  // projections of at least 20M weights below the LM head's width (measured at 7 and 23
-  // rows of the 8B shape: QKV 13.4 -> 11.5 us, gate/up 44.0 -> 39.4, down 24.0 -> 20.1; the
-  // output projection and the LM head stream as fast on the ring).
-  const bool short_tile = mf == 1 && N < 65536 && (int64_t)N * K >= (int64_t)20 << 20;
-  {
-    const int variant = short_tile ? 5 : mf <= 6 ? (N >= 65536 ? 4 : 1) : mf <= 8 ? 13 : mf <= 12 ? 12 : 13;
+  const bool lm_wide = N >= 65536;
+  int variant;
+  if (mf == 1) variant = (int64_t)N * K >= ((int64_t)20 << 20) ? 5 : 0;
+  else if (mf == 2) variant = lm_wide ? 0 : 6;
+  else if (mf <= 4) variant = lm_wide ? 0 : 7;
+  else if (mf == 5) variant = N < 16384 ? 1 : 0;
+  else if (mf == 6) variant = lm_wide ? 4 : 1;
+  else variant = mf <= 8 ? 13 : mf <= 12 ? 12 : 13;
+  if (variant) {
     const TileShape ts = tile_shape(variant);
-    if ((mf >= 6 || short_tile) && K % (16 * ts.ks) == 0) {
+    if (K % (16 * ts.ks) == 0) {
       const int tiles = ((mf * 32 + ts.bm - 1) / ts.bm) * ((N + ts.bn - 1) / ts.bn);
       const int KC = K / (16 * ts.ks);
-      const int s_max = short_tile ? 16 : 8;
+      const int s_max = variant == 5 ? 16 : 8;
       int s = 1;
       while (s < s_max && tiles * s * 2 <= 256 && KC / (s * 2) >= 8) s *= 2;
       const int kcs = (KC + s - 1) / s;

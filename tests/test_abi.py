@@ -190,27 +190,25 @@ def test_binding_rejects_host_and_mistyped_tensors(W):
 
 
 def test_gemm_plan_of_the_wide_projections(W):
-    """Below 6 row fragments the weight ring: 64-column wave tiles (variant 2) for outputs of
-    >= 16384 columns (gate/up and the LM head of the wide test model, d_model 512, d_ff
-    8192, vocabulary 32768), with two K ranges for gate/up, and 32-column tiles below that
-    width.  From 6 fragments the LDS-staged tiles (variant 4) with K split in powers of two
-    while the work items fit one round of 256 workgroups and each split keeps >= 8 chunks:
-    the 8B projections at 171 rows, the 8B / 70B ones at 343 / 370 rows in one 384-row tile,
-    and 1237 rows in 256-row tiles."""
-    gu = W.gemm_plan(44, 2 * 8192, 512)
-    lm = W.gemm_plan(44, 32768, 512)
-    assert gu["kind"] == 2 and lm["kind"] == 2 and gu["rb"] == 1 and lm["rb"] == 1, (gu, lm)
-    assert gu["splits"] == 2, gu
-    assert W.gemm_plan(44, 1024, 256)["kind"] == 1
-    # at most 32 rows: the 32 x 256 tile (up to 16 K ranges) for >= 20M weights below the
-    # LM head's width; the output projection and the LM head stay on the ring
-    for M in (7, 32):
-        assert (W.gemm_plan(M, 6144, 4096)["kind"], W.gemm_plan(M, 6144, 4096)["splits"]) == (4, 8)
-        assert (W.gemm_plan(M, 28672, 4096)["kind"], W.gemm_plan(M, 28672, 4096)["splits"]) == (4, 2)
-        assert (W.gemm_plan(M, 4096, 14336)["kind"], W.gemm_plan(M, 4096, 14336)["splits"]) == (4, 16)
-        assert W.gemm_plan(M, 4096, 4096)["kind"] == 1 and W.gemm_plan(M, 128256, 4096)["kind"] == 2
-    assert W.gemm_plan(33, 6144, 4096)["kind"] == 1
-    cases = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
+    """The launch plan by row fragments (32 rows each).  The weight ring where it streams
+    faster: the output projection at <= 32 rows, the LM head (>= 65536 columns) at 33-160
+    rows, outputs of >= 16384 columns at 129-160 rows (64-column wave tiles, gate/up of the
+    wide test model with two K ranges), small projections at <= 32 rows.  Elsewhere the
+    LDS-staged tiles (variant 4) with K split in powers of two while the work items fit one
+    round of 256 workgroups and each split keeps >= 8 chunks (up to 16 at <= 32 rows)."""
+    ring = {  # (M, N, K): kind
+        (7, 4096, 4096): 1, (7, 1024, 256): 1, (44, 128256, 4096): 2, (150, 128256, 4096): 2,
+        (150, 28672, 4096): 2, (150, 16384, 512): 2, (150, 32768, 512): 2,
+    }
+    for (M, N, K), kind in ring.items():
+        assert W.gemm_plan(M, N, K)["kind"] == kind, (M, N, K, W.gemm_plan(M, N, K))
+    assert W.gemm_plan(150, 16384, 512)["splits"] == 2
+    tiles = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
+        (7, 6144, 4096): (1, 1, 8), (32, 28672, 4096): (1, 1, 2), (7, 4096, 14336): (1, 1, 16),
+        (7, 128256, 4096): (1, 1, 1),
+        (44, 16384, 512): (1, 2, 1), (41, 6144, 4096): (1, 2, 4), (64, 4096, 4096): (1, 2, 8),
+        (87, 28672, 4096): (1, 4, 1), (128, 4096, 14336): (1, 4, 8),
+        (150, 6144, 4096): (1, 6, 4), (150, 4096, 14336): (1, 6, 8),
         (171, 6144, 4096): (1, 6, 4), (171, 4096, 4096): (1, 6, 8), (171, 28672, 4096): (1, 6, 1),
         (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),
         (343, 6144, 4096): (1, 12, 4), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),
@@ -218,7 +216,7 @@ def test_gemm_plan_of_the_wide_projections(W):
         (476, 16384, 512): (2, 8, 1), (680, 16384, 512): (3, 8, 1),
         (1237, 4096, 14336): (5, 8, 1), (1237, 128256, 4096): (5, 8, 1),
     }
-    for (M, N, K), (rb, mt, splits) in cases.items():
+    for (M, N, K), (rb, mt, splits) in tiles.items():
         t = W.gemm_plan(M, N, K)
         assert t["kind"] == 4 and (t["rb"], t["mt"], t["splits"]) == (rb, mt, splits), (M, N, K, t)
     with pytest.raises(W.WispError):

@@ -1,18 +1,17 @@
 """The wide-output projections at the stated bf16 bound.
 
-Below 6 row fragments gate/up and the LM head run the 64-column weight-ring GEMM once
-their output is at least 16384 columns wide, which the 8B / 70B shapes always are and the
-small test models never were.  This model makes both wide at a width the oracle recomputes in seconds: d_model
-512, 8 query heads on 2 kv heads of 64, d_ff 8192 (gate/up 16384 columns), vocabulary
-32768, bf16, 2 layers.  At d_model 512 the gate/up projection is also split over K (two
-ranges summed in fixed order), the LM head is not.
+The 8B / 70B shapes have gate/up and LM-head outputs of at least 16384 columns, which the
+small test models never had.  This model makes both wide at a width the oracle recomputes
+in seconds: d_model 512, 8 query heads on 2 kv heads of 64, d_ff 8192 (gate/up 16384
+columns), vocabulary 32768, bf16, 2 layers.
 
-Cases: 44 rows (the weight-ring GEMMs, gate/up and the LM head on 64-column wave tiles),
-476 and 680 rows (every projection on the LDS-staged 256-row tiles, in two and three row
-tiles).  Checks: logits within 2e-2 max-abs of the oracle, every
-written K/V value within max(two bf16 ulps at its head vector's scale, twice the oracle's floor of its
-layer), untouched slots bit-identical, decisions on the GPU's own logits bit-exact except
-flagged near-ties.
+Cases: 44 rows (every projection on 64 x 128 tiles), 153 rows (gate/up and the LM head on
+the 64-column weight ring, gate/up with two K ranges summed in fixed order; the others on
+192-row tiles), 476 and 680 rows (every projection on 256-row tiles, in two and three row
+tiles).  Checks: logits within 2e-2 max-abs of the oracle, every written K/V value within
+max(two bf16 ulps at its head vector's scale, twice the oracle's floor of its layer),
+untouched slots bit-identical, decisions on the GPU's own logits bit-exact except flagged
+near-ties.
 """
 import numpy as np
 import pytest
@@ -27,11 +26,11 @@ WIDE_BF16 = wi.ModelShape("wide-bf16", 2, 512, 8, 2, 64, 8192, 32768, "bf16", 10
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("B", [8, 28, 40], ids=["44rows", "476rows", "680rows"])
+@pytest.mark.parametrize("B", [8, 9, 28, 40], ids=["44rows", "153rows", "476rows", "680rows"])
 def test_wide_projections_match_the_oracle(B):
     r = np.random.default_rng(8192 + B)
     ctx = r.integers(0, 64, size=B).astype(np.int32)
-    # 8 requests of 36 drafts in all: 44 rows; B requests of 16 drafts: 17 B rows
+    # 8 requests of 36 drafts in all: 44 rows; otherwise B requests of 16 drafts: 17 B rows
     gamma = np.array([7, 1, 5, 3, 6, 4, 2, 8] if B == 8 else [16] * B, np.int32)
     mix = wi.custom_mix(WIDE_BF16, ctx, gamma, kv_source="prefill", name=f"wide-{B}", t_draft=1.0,
                         sigma=0.5)
