@@ -63,15 +63,18 @@ typedef enum { WISP_F32 = 0, WISP_BF16 = 1 } wisp_dtype;
  *   final_norm, attn_norm[l], mlp_norm[l]  [d_model]
  *   w_qkv[l]    rows (n_q + 2 n_kv) * head_dim  (W_q rows, then W_k, then W_v), K = d_model
  *   w_o[l]      rows d_model,   K = n_q * head_dim
- *   w_gate_up[l] rows 2 * d_ff (W_gate rows, then W_up), K = d_model
+ *   w_gate_up[l] rows 2 * d_ff, K = d_model: W_gate and W_up packed together by
+ *               wisp_pack_gate_up (for WISP_BF16 their 32-row blocks interleave, so one
+ *               output tile holds both halves of each SwiGLU pair; WISP_F32: W_gate rows,
+ *               then W_up)
  *   w_down[l]   rows d_model,   K = d_ff
  *   lm_head     rows vocab,     K = d_model
  * Shapes: d_model and d_ff multiples of 32, d_model <= 8192; head_dim a multiple of 32 up
  * to 256 (64 or 128 for WISP_BF16), n_q_heads a multiple of n_kv_heads; for WISP_BF16 also vocab a
  * multiple of 32 and at most 64 query heads per kv head.  Others: WISP_E_UNSUPPORTED.
  * Linear weights ("rows x K", nn.Linear's [out][in]) must be stored in the packed
- * form made by wisp_pack_linear(): for WISP_BF16 an MFMA-fragment order, for
- * WISP_F32 plain row-major.
+ * form made by wisp_pack_linear() (wisp_pack_gate_up() for w_gate_up): for WISP_BF16 an
+ * MFMA-fragment order, for WISP_F32 plain row-major.
  */
 typedef struct {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
@@ -147,6 +150,19 @@ size_t wisp_logits_workspace_size(const wisp_model *model, const wisp_batch_desc
  */
 wisp_status wisp_pack_linear(void *dst, const void *src, int32_t rows, int32_t cols, int32_t dtype,
                              void *stream);
+
+/*
+ * Pack the MLP's gate and up weights (natural [d_ff][d_model] row-major each, DEVICE) into
+ * w_gate_up (DEVICE, 2 * d_ff * d_model elements; must not alias the sources).
+ * WISP_BF16: d_ff % 32 == 0 and d_model % 16 == 0; the fragment order of wisp_pack_linear
+ * over 2 * d_ff rows whose 32-row blocks interleave, block 2b holding W_gate rows
+ * 32b .. 32b + 31 and block 2b + 1 the W_up rows of the same b.  An output tile of the
+ * gate/up projection then holds gate and up of the same columns, and the step applies
+ * SwiGLU (silu(gate) * up, Sec. 4.5's target model) in that projection's epilogue.
+ * WISP_F32: W_gate rows, then W_up rows (plain copies).
+ */
+wisp_status wisp_pack_gate_up(void *dst, const void *w_gate, const void *w_up, int32_t d_ff, int32_t d_model,
+                              int32_t dtype, void *stream);
 
 /*
  * The verification step (Sec. 4.5): forward + acceptance, returns L and the extra token.

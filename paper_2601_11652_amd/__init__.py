@@ -38,7 +38,8 @@ ROWS_MAX = 262144
 TAG_ACCEPT = 1
 TAG_RACE = 2
 
-EXPORTS = ("wisp_workspace_size", "wisp_logits_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear", "wisp_verify",
+EXPORTS = ("wisp_workspace_size", "wisp_logits_workspace_size", "wisp_accept_workspace_size", "wisp_pack_linear",
+           "wisp_pack_gate_up", "wisp_verify",
            "wisp_accept", "wisp_attention", "wisp_uniform", "wisp_check", "wisp_profile_enable",
            "wisp_profile_read", "wisp_profile_reset", "wisp_last_error", "wisp_schedule", "wisp_kvm_create",
            "wisp_kvm_destroy", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit", "wisp_kvm_release",
@@ -123,6 +124,7 @@ def _load():
     L.wisp_accept_workspace_size.argtypes = [C.POINTER(wisp_batch_desc), C.c_int32]
     L.wisp_accept_workspace_size.restype = C.c_size_t
     L.wisp_pack_linear.argtypes = [_VP, _VP, C.c_int32, C.c_int32, C.c_int32, _VP]
+    L.wisp_pack_gate_up.argtypes = [_VP, _VP, _VP, C.c_int32, C.c_int32, C.c_int32, _VP]
     L.wisp_verify.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
                               _VP, _VP, C.c_uint64, _VP, _VP, _VP, _VP, C.c_size_t, _VP]
     L.wisp_verify_noalloc.argtypes = [C.POINTER(wisp_model), C.POINTER(wisp_kv), C.POINTER(wisp_batch_desc),
@@ -156,7 +158,7 @@ def _load():
     L.wisp_draft_stats_workspace_size.restype = C.c_size_t
     L.wisp_draft_stats.argtypes = [_VP, C.c_int32, C.c_int32, C.c_int64, C.c_float, _VP, _VP, C.c_size_t, _VP]
     L.wisp_reject_predict.argtypes = [C.POINTER(wisp_reject_mlp), _VP, C.c_int32, _VP, _VP]
-    for name in ("wisp_pack_linear", "wisp_verify", "wisp_verify_noalloc", "wisp_accept", "wisp_attention", "wisp_uniform",
+    for name in ("wisp_pack_linear", "wisp_pack_gate_up", "wisp_verify", "wisp_verify_noalloc", "wisp_accept", "wisp_attention", "wisp_uniform",
                  "wisp_check", "wisp_gemm_plan", "wisp_profile_enable", "wisp_profile_read", "wisp_profile_reset",
                  "wisp_schedule", "wisp_kvm_create", "wisp_kvm_lookup", "wisp_kvm_reserve", "wisp_kvm_commit",
                  "wisp_kvm_release", "wisp_kvm_get_stats", "wisp_draft_stats", "wisp_reject_predict"):
@@ -337,8 +339,9 @@ class GpuModel:
             wo = torch.empty(s.d_model * qd, dtype=dt, device=dev)
             pack(wo, w["wo"], s.d_model, qd)
             gu = torch.empty(2 * s.d_ff * s.d_model, dtype=dt, device=dev)
-            pack(gu, w["w_gate"], s.d_ff, s.d_model, 0)
-            pack(gu, w["w_up"], s.d_ff, s.d_model, s.d_ff)
+            for x in ("w_gate", "w_up"):
+                assert w[x].is_contiguous() and w[x].dtype == dt and tuple(w[x].shape) == (s.d_ff, s.d_model)
+            wisp_pack_gate_up(gu, w["w_gate"], w["w_up"], s.d_ff, s.d_model, code, stream)
             wd = torch.empty(s.d_model * s.d_ff, dtype=dt, device=dev)
             pack(wd, w["w_down"], s.d_model, s.d_ff)
             self.layers.append({"attn_norm": w["attn_norm"].contiguous(), "mlp_norm": w["mlp_norm"].contiguous(),
@@ -392,6 +395,13 @@ def wisp_pack_linear(dst, src, rows: int, cols: int, dtype: int, stream=None):
     n = max(rows, 0) * max(cols, 0)
     _ok(lib.wisp_pack_linear(_dev(dst, "dst", n, elem=es), _dev(src, "src", n, elem=es), rows, cols, dtype,
                              _stream(stream)))
+
+
+def wisp_pack_gate_up(dst, w_gate, w_up, d_ff: int, d_model: int, dtype: int, stream=None):
+    es = 2 if dtype == WISP_BF16 else 4
+    n = max(d_ff, 0) * max(d_model, 0)
+    _ok(lib.wisp_pack_gate_up(_dev(dst, "dst", 2 * n, elem=es), _dev(w_gate, "w_gate", n, elem=es),
+                              _dev(w_up, "w_up", n, elem=es), d_ff, d_model, dtype, _stream(stream)))
 
 
 def _ws(workspace) -> tuple[int, int]:

@@ -159,6 +159,16 @@ struct RowMaxOut {
   int tiles;
 };
 
+// The gate/up projection's epilogue output: silu(gate) * up of each row, stored as bf16
+// in the fragment-packed input layout of the down projection (K = F).
+struct SwigluOut {
+  uint16_t *out;
+  int F;
+};
+// SwiGLU's elementwise step, shared by the SwiGLU kernel and the GEMM epilogue so that both
+// give bit-identical results
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + expf(-g)) * u; }
+
 // Each row's maximum over one output tile's columns, and the first column holding it, from
 // the fp32 accumulators just stored (the LM head's logits).  Lane l of a wave holds column
 // l % 32 of each of its fragments for rows 4 (l / 32) + 8 (e / 4) + e % 4; a row's values

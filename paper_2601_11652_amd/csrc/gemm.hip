@@ -318,9 +318,9 @@ static void launch_ring(int mt, dim3 grid, const uint16_t *A, const uint16_t *W,
 }
 
 void gemm_bf16(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
-               const GemmCfg &cfg, hipStream_t s, RowMaxOut rm) {
+               const GemmCfg &cfg, hipStream_t s, RowMaxOut rm, SwigluOut sw) {
   if (cfg.kind == 4) {
-    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, cfg.kf_per_split / tile_shape(cfg.variant).ks, rm, s);
+    gemm_bf16_tile(A, W, C, M, N, K, ldc, cfg.variant, cfg.kf_per_split / tile_shape(cfg.variant).ks, rm, s, sw);
     return;
   }
   dim3 grid(((N + cfg.bn - 1) / cfg.bn) * cfg.splits, cfg.rb, 1);
@@ -381,22 +381,34 @@ void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int
 // weight packing: natural [rows][cols] -> 32x16 fragments
 // ---------------------------------------------------------------------------------------
 __global__ void pack_bf16_kernel(uint16_t *__restrict__ dst, const uint16_t *__restrict__ src,
-                                 int rows, int cols) {
-  // one thread per (row, 8-column chunk): 16 contiguous bytes in, 16 contiguous bytes out
+                                 int rows, int cols, int blk_mul, int blk_add) {
+  // one thread per (row, 8-column chunk): 16 contiguous bytes in, 16 contiguous bytes out;
+  // source row r goes to packed row ((r / 32) * blk_mul + blk_add) * 32 + r % 32
   const int64_t chunks = (int64_t)rows * (cols / 8);
   for (int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; c < chunks;
        c += (int64_t)gridDim.x * blockDim.x) {
     const int64_t r = c / (cols / 8), k = (c % (cols / 8)) * 8;
+    const int64_t rd = ((r >> 5) * blk_mul + blk_add) * 32 + (r & 31);
     const uint4 v = *reinterpret_cast<const uint4 *>(src + r * cols + k);
-    *reinterpret_cast<uint4 *>(dst + packed_off(r, k, cols)) = v;
+    *reinterpret_cast<uint4 *>(dst + packed_off(rd, k, cols)) = v;
   }
 }
 
-void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hipStream_t s) {
+static void pack_rows(uint16_t *dst, const uint16_t *src, int rows, int cols, int blk_mul, int blk_add,
+                      hipStream_t s) {
   const int64_t chunks = (int64_t)rows * (cols / 8);
   int blocks = (int)((chunks + 255) / 256);
   if (blocks > 65535) blocks = 65535;
-  launch(pack_bf16_kernel, blocks, 256, 0, s, dst, src, rows, cols);
+  launch(pack_bf16_kernel, blocks, 256, 0, s, dst, src, rows, cols, blk_mul, blk_add);
+}
+
+void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hipStream_t s) {
+  pack_rows(dst, src, rows, cols, 1, 0, s);
+}
+
+void pack_gate_up_bf16(uint16_t *dst, const uint16_t *gate, const uint16_t *up, int F, int d, hipStream_t s) {
+  pack_rows(dst, gate, F, d, 2, 0, s);
+  pack_rows(dst, up, F, d, 2, 1, s);
 }
 
 }  // namespace wisp

@@ -52,12 +52,12 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int WGM, int WGN, int MTW, int NTW, int KS, int ST, bool RM>
+template <int WGM, int WGN, int MTW, int NTW, int KS, int ST, bool RM, bool SW>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_t *__restrict__ A,
                                                         const uint16_t *__restrict__ W,
                                                         float *__restrict__ C, int M, int N, int K,
                                                         int ldc, int tiles_m, int tiles, int per_xcd,
-                                                        int kc_split, RowMaxOut rmax) {
+                                                        int kc_split, RowMaxOut rmax, SwigluOut sw) {
   constexpr int NW = WGM * WGN;               // waves
   constexpr int AF = WGM * MTW, BF = WGN * NTW;   // A / W fragments of the tile per K step
   constexpr int SF = (AF + BF) * KS;          // fragments per stage
@@ -188,6 +188,51 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
     });
 
   wait_vmcnt<0>();
+  if constexpr (SW) {
+    // gate/up projection with its weights packed by wisp_pack_gate_up: column fragment 2b
+    // holds gate columns 32b .. 32b + 31 and fragment 2b + 1 the up columns of the same b,
+    // so silu(gate) * up of column j = 32b + (lane % 32) pairs fragments 2b and 2b + 1 at
+    // the same lane and accumulator element.  The tile's first fragment is even (BF is).
+    static_assert(BF % 2 == 0, "gate/up fragment pairs stay inside one tile");
+    auto emit = [&](int i, int nb_gate, const floatx16 &g, const floatx16 &u) {
+      if (nb_gate >= NF) return;
+      const int rbase = (rb0 + wm * MTW + i) * 32 + 4 * (lane >> 5);
+      const int j = (nb_gate >> 1) * 32 + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = rbase + 8 * (e >> 2) + (e & 3);
+        if (row < M) sw.out[packed_off(row, j, sw.F)] = f2bf(silu_mul(g[e], u[e]));
+      }
+    };
+    if constexpr (NTW % 2 == 0) {   // both fragments of a pair in this wave's registers
+#pragma unroll
+      for (int i = 0; i < MTW; ++i)
+#pragma unroll
+        for (int q = 0; q < NTW; q += 2) emit(i, nb0 + wn * NTW + q, acc[i][q], acc[i][q + 1]);
+    } else {
+      // one fragment per wave: wave wn + 1 (odd) holds the up half of wave wn's gate
+      // fragment; it hands its accumulators over through LDS, one row fragment at a time
+      static_assert(NTW == 1 && WGN % 2 == 0, "gate/up pairs across neighbouring waves");
+      static_assert(WGM * (WGN / 2) * 16 * 64 * 4 <= SF * 1024, "the exchange fits one stage buffer");
+      float *x = reinterpret_cast<float *>(&lds0[0][0]) + ((wm * (WGN / 2) + (wn >> 1)) * 16) * 64 + lane;
+#pragma unroll
+      for (int i = 0; i < MTW; ++i) {
+        __syncthreads();   // every wave is done with the stage buffers / the previous round
+        if (wn & 1) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) x[e * 64] = acc[i][0][e];
+        }
+        __syncthreads();
+        if (!(wn & 1)) {
+          floatx16 u;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) u[e] = x[e * 64];
+          emit(i, nb0 + wn, acc[i][0], u);
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MTW; ++i) {
     const int rbase = (rb0 + wm * MTW + i) * 32 + 4 * (lane >> 5);
@@ -213,7 +258,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_tile_kernel(const uint16_
 
 template <int WGM, int WGN, int MTW, int NTW, int KS, int ST>
 static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc,
-                        RowMaxOut rm, hipStream_t s, int kc_split) {
+                        RowMaxOut rm, hipStream_t s, int kc_split, SwigluOut sw) {
   static_assert(2 * WGN * WGM * MTW * 32 * 4 <= (WGM * MTW + WGN * NTW) * KS * 1024,
                 "the row-maxima exchange fits one stage buffer");
   const int tiles_m = ((M + 31) / 32 + WGM * MTW - 1) / (WGM * MTW);
@@ -222,11 +267,14 @@ static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, i
   const int splits = (KC + kc_split - 1) / kc_split;
   const int tiles = tiles_m * tiles_n, per_xcd = (tiles * splits + 7) / 8;
   if (rm.m)
-    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, true>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K,
-           ldc, tiles_m, tiles, per_xcd, kc_split, rm);
+    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, true, false>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M,
+           N, K, ldc, tiles_m, tiles, per_xcd, kc_split, rm, sw);
+  else if (sw.out)
+    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, false, true>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M,
+           N, K, ldc, tiles_m, tiles, per_xcd, kc_split, rm, sw);
   else
-    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, false>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M, N, K,
-           ldc, tiles_m, tiles, per_xcd, kc_split, rm);
+    launch(gemm_tile_kernel<WGM, WGN, MTW, NTW, KS, ST, false, false>, 8 * per_xcd, 64 * WGM * WGN, 0, s, A, W, C, M,
+           N, K, ldc, tiles_m, tiles, per_xcd, kc_split, rm, sw);
 }
 
 // Tile shapes (measured at 7-1237 rows of the 8B and 70B projections, cold weights):
@@ -249,15 +297,15 @@ TileShape tile_shape(int variant) {
 }
 
 void gemm_bf16_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N, int K, int ldc, int variant,
-                    int kc_split, RowMaxOut rm, hipStream_t s) {
+                    int kc_split, RowMaxOut rm, hipStream_t s, SwigluOut sw) {
   switch (variant) {
-    case 1: launch_tile<2, 4, 3, 1, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
-    case 4: launch_tile<2, 4, 3, 2, 4, 2>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
-    case 12: launch_tile<4, 2, 3, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
-    case 13: launch_tile<4, 2, 2, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
-    case 5: launch_tile<1, 4, 1, 2, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;   // 4 waves
-    case 6: launch_tile<2, 4, 1, 1, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
-    case 7: launch_tile<4, 2, 1, 2, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split); break;
+    case 1: launch_tile<2, 4, 3, 1, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 4: launch_tile<2, 4, 3, 2, 4, 2>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 12: launch_tile<4, 2, 3, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 13: launch_tile<4, 2, 2, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 5: launch_tile<1, 4, 1, 2, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;   // 4 waves
+    case 6: launch_tile<2, 4, 1, 1, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 7: launch_tile<4, 2, 1, 2, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
   }
 }
 

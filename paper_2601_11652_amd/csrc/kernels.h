@@ -38,7 +38,8 @@ struct GemmCfg {
 };
 GemmCfg gemm_bf16_plan(int M, int N, int K);
 void gemm_bf16(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K,
-               int ldc, const GemmCfg &cfg, hipStream_t s, RowMaxOut rm = RowMaxOut{nullptr, nullptr, 0});
+               int ldc, const GemmCfg &cfg, hipStream_t s, RowMaxOut rm = RowMaxOut{nullptr, nullptr, 0},
+               SwigluOut sw = SwigluOut{nullptr, 0});
 void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int ldc, hipStream_t s);
 // LDS-staged output tiles (both operands staged through LDS): variant 1 is 192 x 128,
 // 4 is 192 x 256, 6 is 64 x 128, 7 is 128 x 128, 12 is 384 x 128 and 13 is 256 x 128
@@ -48,8 +49,11 @@ void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int
 struct TileShape { int bm, bn, ks; };
 TileShape tile_shape(int variant);
 void gemm_bf16_tile(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int M, int N, int K, int ldc,
-                    int variant, int kc_split, RowMaxOut rm, hipStream_t s);
+                    int variant, int kc_split, RowMaxOut rm, hipStream_t s, SwigluOut sw = SwigluOut{nullptr, 0});
 void pack_linear_bf16(uint16_t *dst, const uint16_t *src, int rows, int cols, hipStream_t s);
+// gate/up weights ([F][d] each) packed with their 32-row blocks interleaved: packed row
+// block 2b = gate rows 32b .. 32b + 31, 2b + 1 = the up rows of the same b
+void pack_gate_up_bf16(uint16_t *dst, const uint16_t *gate, const uint16_t *up, int F, int d, hipStream_t s);
 
 // ----- per-row layers --------------------------------------------------------------------
 struct StepDesc {         // device arrays carved from the workspace
@@ -86,7 +90,7 @@ void qkv_rope_append(const StepDesc &d, const float *part, int splits, const flo
                      T *k_pool, T *v_pool, int M, int nq, int nkv, int hd, hipStream_t s);
 
 template <typename T>
-void swiglu(const float *part, int splits, T *out, bool packed, int M, int F, hipStream_t s);
+void swiglu(const float *part, int splits, T *out, bool packed, int M, int F, bool interleaved, hipStream_t s);
 
 // ----- attention ---------------------------------------------------------------------------
 struct AttnItem {   // one wave's work: request, kv head, row group, token range

@@ -297,37 +297,43 @@ void qkv_rope_append(const StepDesc &d, const float *part, int splits, const flo
 }
 
 // ---------------------------------------------------------------------------------------
-// SwiGLU: silu(gate) * up, gate/up are columns [0, F) and [F, 2F) of the partials
+// SwiGLU: silu(gate) * up.  Gate/up partials are either stacked (columns [0, F) and
+// [F, 2F): the fp32 path) or interleaved by 32-column fragments (bf16 weights packed by
+// wisp_pack_gate_up: fragment 2b holds gate columns 32b .. 32b + 31, fragment 2b + 1 the
+// up columns of the same b)
 // ---------------------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_kernel(const float *__restrict__ part, int splits,
-                                                     T *__restrict__ out, bool packed, int M, int F) {
+                                                     T *__restrict__ out, bool packed, int M, int F,
+                                                     bool interleaved) {
   const int64_t chunks = (int64_t)M * (F / 8);
   const int64_t stride = (int64_t)M * 2 * F;
   for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < chunks;
        t += (int64_t)gridDim.x * blockDim.x) {
     const int64_t r = t / (F / 8), c = (t % (F / 8)) * 8;
     const float *pr = part + r * 2 * F;
+    const int64_t gc = interleaved ? (c / 32) * 64 + c % 32 : c;
+    const int64_t uc = interleaved ? gc + 32 : F + c;
     float4 g[2], u[2];
-    g[0] = sum_splits4(pr + c, stride, splits);
-    g[1] = sum_splits4(pr + c + 4, stride, splits);
-    u[0] = sum_splits4(pr + F + c, stride, splits);
-    u[1] = sum_splits4(pr + F + c + 4, stride, splits);
+    g[0] = sum_splits4(pr + gc, stride, splits);
+    g[1] = sum_splits4(pr + gc + 4, stride, splits);
+    u[0] = sum_splits4(pr + uc, stride, splits);
+    u[1] = sum_splits4(pr + uc + 4, stride, splits);
     const float gv[8] = {g[0].x, g[0].y, g[0].z, g[0].w, g[1].x, g[1].y, g[1].z, g[1].w};
     const float uv[8] = {u[0].x, u[0].y, u[0].z, u[0].w, u[1].x, u[1].y, u[1].z, u[1].w};
     float v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = gv[e] / (1.0f + expf(-gv[e])) * uv[e];
+    for (int e = 0; e < 8; ++e) v[e] = silu_mul(gv[e], uv[e]);
     store8<T>(out, packed, r, c, F, v);
   }
 }
 
 template <typename T>
-void swiglu(const float *part, int splits, T *out, bool packed, int M, int F, hipStream_t s) {
+void swiglu(const float *part, int splits, T *out, bool packed, int M, int F, bool interleaved, hipStream_t s) {
   const int64_t chunks = (int64_t)M * (F / 8);
   int blocks = (int)((chunks + 255) / 256);
   if (blocks > 4096) blocks = 4096;
-  launch(swiglu_kernel<T>, blocks, 256, 0, s, part, splits, out, packed, M, F);
+  launch(swiglu_kernel<T>, blocks, 256, 0, s, part, splits, out, packed, M, F, interleaved);
 }
 
 template void embed_norm<float>(const StepDesc &, const float *, const float *, const int32_t *,
@@ -344,7 +350,7 @@ template void qkv_rope_append<float>(const StepDesc &, const float *, int, const
 template void qkv_rope_append<uint16_t>(const StepDesc &, const float *, int, const float *,
                                         uint16_t *, uint16_t *, uint16_t *, int, int, int, int,
                                         hipStream_t);
-template void swiglu<float>(const float *, int, float *, bool, int, int, hipStream_t);
-template void swiglu<uint16_t>(const float *, int, uint16_t *, bool, int, int, hipStream_t);
+template void swiglu<float>(const float *, int, float *, bool, int, int, bool, hipStream_t);
+template void swiglu<uint16_t>(const float *, int, uint16_t *, bool, int, int, bool, hipStream_t);
 
 }  // namespace wisp

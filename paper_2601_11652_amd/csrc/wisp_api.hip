@@ -567,10 +567,16 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
       ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
       resid_norm<T>(part, so, h, (const T *)m->mlp_norm[l], xn, packed, p.M, p.d, m->rms_eps, s);
     }
-    const int sg = gemm(xn, m->w_gate_up[l], part, 2 * p.F, p.d, p.g_gu);
-    {
+    if (p.bf16 && p.g_gu.kind == 4 && p.g_gu.splits == 1) {
+      // one K range on the tile kernel: SwiGLU in the GEMM's epilogue, which writes the down
+      // projection's bf16 input directly (no fp32 gate/up round trip, no SwiGLU launch)
+      ProfScope ps(gemm_class(p, p.g_gu), gemm_bytes(2 * p.F, p.d), gemm_flops(2 * p.F, p.d), s);
+      gemm_bf16((const uint16_t *)xn, (const uint16_t *)m->w_gate_up[l], part, p.M, 2 * p.F, p.d, 2 * p.F, p.g_gu,
+                s, RowMaxOut{nullptr, nullptr, 0}, SwigluOut{(uint16_t *)af, p.F});
+    } else {
+      const int sg = gemm(xn, m->w_gate_up[l], part, 2 * p.F, p.d, p.g_gu);
       ProfScope ps(WISP_PROF_ROWS, 0, 0, s);
-      swiglu<T>(part, sg, af, packed, p.M, p.F, s);
+      swiglu<T>(part, sg, af, packed, p.M, p.F, p.bf16, s);   // bf16 gate/up: interleaved columns
     }
     const int sdn = gemm(af, m->w_down[l], part, p.d, p.F, p.g_down);
     const bool last = l + 1 == m->n_layers;
@@ -749,6 +755,28 @@ size_t wisp_accept_workspace_size(const wisp_batch_desc *desc, int32_t vocab) {
     Plan p;
     if (make_plan(p, nullptr, desc, false, vocab) != WISP_OK) return 0;
     return p.total;
+  });
+}
+
+wisp_status wisp_pack_gate_up(void *dst, const void *w_gate, const void *w_up, int32_t d_ff, int32_t d_model,
+                              int32_t dtype, void *stream) {
+  return guarded("wisp_pack_gate_up", [&]() -> wisp_status {
+    if (!dst || !w_gate || !w_up) return fail(WISP_E_INVALID, "NULL pointer");
+    if (d_ff <= 0 || d_model <= 0) return fail(WISP_E_INVALID, "d_ff, d_model must be positive");
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == WISP_BF16) {
+      if (d_ff % 32 || d_model % 16)
+        return fail(WISP_E_UNSUPPORTED, "bf16 packing needs d_ff %% 32 == 0 and d_model %% 16 == 0");
+      pack_gate_up_bf16((uint16_t *)dst, (const uint16_t *)w_gate, (const uint16_t *)w_up, d_ff, d_model, s);
+    } else if (dtype == WISP_F32) {
+      const size_t half = (size_t)d_ff * d_model * 4;
+      if (hipMemcpyAsync(dst, w_gate, half, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+          hipMemcpyAsync((char *)dst + half, w_up, half, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return fail(WISP_E_HIP, "copy failed");
+    } else {
+      return fail(WISP_E_UNSUPPORTED, "dtype %d", dtype);
+    }
+    return hip_check("pack");
   });
 }
 

@@ -151,6 +151,11 @@ def test_workspace_size_and_pack_validation(W):
     assert L.wisp_pack_linear(FAKE, FAKE, 32, 8, W.WISP_BF16, None) == W.WISP_E_UNSUPPORTED
     assert L.wisp_pack_linear(None, FAKE, 32, 16, W.WISP_BF16, None) == W.WISP_E_INVALID
     assert L.wisp_pack_linear(FAKE, FAKE, 32, 16, 7, None) == W.WISP_E_UNSUPPORTED
+    assert L.wisp_pack_gate_up(FAKE, FAKE, FAKE, 48, 64, W.WISP_BF16, None) == W.WISP_E_UNSUPPORTED
+    assert L.wisp_pack_gate_up(FAKE, FAKE, FAKE, 64, 8, W.WISP_BF16, None) == W.WISP_E_UNSUPPORTED
+    assert L.wisp_pack_gate_up(FAKE, None, FAKE, 64, 64, W.WISP_BF16, None) == W.WISP_E_INVALID
+    assert L.wisp_pack_gate_up(FAKE, FAKE, FAKE, 0, 64, W.WISP_BF16, None) == W.WISP_E_INVALID
+    assert L.wisp_pack_gate_up(FAKE, FAKE, FAKE, 64, 64, 7, None) == W.WISP_E_UNSUPPORTED
 
 
 def test_logits_in_workspace_sizes(W):
