@@ -224,7 +224,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(StepDesc d, const AttnIt
 // Fixed-order combine of each group's chunk partials: one thread per (row, 8 head dims).
 // Pass 1 takes the maximum of the chunks' running maxima, pass 2 adds the rescaled chunk
 // sums in chunk order.  Each pass loads MAXC chunks' values before using any of them, so
-// a group of up to MAXC chunks costs two memory round trips rather than one per chunk.
+// a longer group costs two memory round trips per MAXC chunks; a group of at most MAXC
+// chunks loads everything in one round.
 // Writes the bf16 attention output of each (row, q head) into the O-projection's input
 // layout.
 template <int HD, int MAXC>
@@ -251,18 +252,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
 
   // a group's threads fill whole waves (UNITS is a multiple of 64), so `cb + c < n` is
   // wave-uniform: chunks past the group's last are not loaded at all
-  float m = -INFINITY;
-  for (int cb = 0; cb < n; cb += MAXC) {
-    float mc[MAXC];
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c) mc[c] = cb + c < n ? part_ml[(item_of(cb + c) * 64 + rr) * 2] : -INFINITY;
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (cb + c < n) m = fmaxf(m, mc[c]);
-  }
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float den = 0.f;
-  for (int cb = 0; cb < n; cb += MAXC) {
+  float m = -INFINITY;
+  if (n <= MAXC) {
+    // one round of loads: every chunk's (m, l) and O values at once, the maximum taken from
+    // registers; the same sums in the same order as the two-pass form below
     float mc[MAXC], lc[MAXC], pv[MAXC][8];
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
@@ -270,8 +265,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
       lc[c] = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pv[c][e] = 0.f;
-      if (cb + c < n) {
-        const int64_t itm = item_of(cb + c);
+      if (c < n) {
+        const int64_t itm = item_of(c);
         mc[c] = part_ml[(itm * 64 + rr) * 2];
         lc[c] = part_ml[(itm * 64 + rr) * 2 + 1];
         const float *po = part_o + (itm * HD + c0) * 64 + rr;
@@ -280,12 +275,50 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(StepDesc d, const Att
       }
     }
 #pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (c < n) m = fmaxf(m, mc[c]);
+#pragma unroll
     for (int c = 0; c < MAXC; ++c) {
-      if (cb + c >= n || mc[c] == -INFINITY) continue;
+      if (c >= n || mc[c] == -INFINITY) continue;
       const float w = expf(mc[c] - m);
       den += lc[c] * w;
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[e] += pv[c][e] * w;
+    }
+  } else {
+    for (int cb = 0; cb < n; cb += MAXC) {
+      float mc[MAXC];
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) mc[c] = cb + c < n ? part_ml[(item_of(cb + c) * 64 + rr) * 2] : -INFINITY;
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c)
+        if (cb + c < n) m = fmaxf(m, mc[c]);
+    }
+    for (int cb = 0; cb < n; cb += MAXC) {
+      float mc[MAXC], lc[MAXC], pv[MAXC][8];
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) {
+        mc[c] = -INFINITY;
+        lc[c] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pv[c][e] = 0.f;
+        if (cb + c < n) {
+          const int64_t itm = item_of(cb + c);
+          mc[c] = part_ml[(itm * 64 + rr) * 2];
+          lc[c] = part_ml[(itm * 64 + rr) * 2 + 1];
+          const float *po = part_o + (itm * HD + c0) * 64 + rr;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pv[c][e] = po[e * 64];
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c) {
+        if (cb + c >= n || mc[c] == -INFINITY) continue;
+        const float w = expf(mc[c] - m);
+        den += lc[c] * w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += pv[c][e] * w;
+      }
     }
   }
   const int lr = lr0 + rr;
