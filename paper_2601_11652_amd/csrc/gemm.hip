@@ -228,7 +228,11 @@ static constexpr int kPairedWavesMinMT = 5;
 //   6: 192-row tiles, 256 columns wide only for the LM head (measured over whole steps: for
 //     gate/up the 128-column tile in one K range costs the same and halves the partial sums
 //     the SwiGLU kernel reads);
-//   7-8: one 256-row tile, 9-12: one 384-row tile, beyond: 256-row tiles.
+//   7-8: one 256-row tile, 9-12: one 384-row tile;
+//   beyond (> 384 rows): 256 x 256 tiles for outputs of >= 16384 columns (gate/up, LM head:
+//     6-13 % faster than 256 x 128 at 512-1237 rows), else 384- or 256-row tiles of 128
+//     columns, whichever pads fewer rows (at 680 rows 384-row tiles: QKV 66 -> 51 us, down
+//     117 -> 99).
 // K is split in powers of two while the work items fit one round of 256 workgroups and
 // each split keeps at least 8 chunks (fewer splits cost the GEMMs more than the row
 // kernels save).  The ring holds all rows of a row block of at most 256 rows: 64-column
@@ -245,7 +249,10 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   else if (mf <= 4) variant = lm_wide ? 0 : 7;
   else if (mf == 5) variant = N < 16384 ? 1 : 0;
   else if (mf == 6) variant = lm_wide ? 4 : 1;
-  else variant = mf <= 8 ? 13 : mf <= 12 ? 12 : 13;
+  else if (mf <= 8) variant = 13;
+  else if (mf <= 12) variant = 12;
+  else if (N >= 16384) variant = 17;
+  else variant = (mf + 11) / 12 * 12 <= (mf + 7) / 8 * 8 ? 12 : 13;   // the tile that pads fewer rows
   if (variant) {
     const TileShape ts = tile_shape(variant);
     if (K % (16 * ts.ks) == 0) {

@@ -292,6 +292,7 @@ TileShape tile_shape(int variant) {
     case 5: return {32, 256, 4};
     case 6: return {64, 128, 4};
     case 7: return {128, 128, 4};
+    case 17: return {256, 256, 2};
   }
   return {0, 0, 0};
 }
@@ -306,6 +307,7 @@ void gemm_bf16_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N
     case 5: launch_tile<1, 4, 1, 2, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;   // 4 waves
     case 6: launch_tile<2, 4, 1, 1, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
     case 7: launch_tile<4, 2, 1, 2, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 17: launch_tile<2, 4, 4, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
   }
 }
 

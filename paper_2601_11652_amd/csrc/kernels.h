@@ -42,8 +42,8 @@ void gemm_bf16(const uint16_t *A_packed, const uint16_t *W_packed, float *C, int
                SwigluOut sw = SwigluOut{nullptr, 0});
 void gemm_f32(const float *A, const float *W, float *C, int M, int N, int K, int ldc, hipStream_t s);
 // LDS-staged output tiles (both operands staged through LDS): variant 1 is 192 x 128,
-// 4 is 192 x 256, 6 is 64 x 128, 7 is 128 x 128, 12 is 384 x 128 and 13 is 256 x 128
-// (rows x columns, 8 waves), 5 is 32 x 256 (4 waves).  K is
+// 4 is 192 x 256, 6 is 64 x 128, 7 is 128 x 128, 12 is 384 x 128, 13 is 256 x 128 and
+// 17 is 256 x 256 (rows x columns, 8 waves), 5 is 32 x 256 (4 waves).  K is
 // cut into chunks of 16 ks (ks = tile_k_steps(variant)); a work item sums kc_split chunks
 // into its own fp32 partial C[z] (z = its K range), C[0] alone when kc_split covers K.
 struct TileShape { int bm, bn, ks; };

@@ -200,7 +200,9 @@ def test_gemm_plan_of_the_wide_projections(W):
     rows, outputs of >= 16384 columns at 129-160 rows (64-column wave tiles, gate/up of the
     wide test model with two K ranges), small projections at <= 32 rows.  Elsewhere the
     LDS-staged tiles (variant 4) with K split in powers of two while the work items fit one
-    round of 256 workgroups and each split keeps >= 8 chunks (up to 16 at <= 32 rows)."""
+    round of 256 workgroups and each split keeps >= 8 chunks (up to 16 at <= 32 rows);
+    beyond 384 rows 256 x 256 tiles for outputs of >= 16384 columns, else the 384- or
+    256-row tiles, whichever pads fewer rows."""
     ring = {  # (M, N, K): kind
         (7, 4096, 4096): 1, (7, 1024, 256): 1, (44, 128256, 4096): 2, (150, 128256, 4096): 2,
         (150, 28672, 4096): 2, (150, 16384, 512): 2, (150, 32768, 512): 2,
@@ -218,7 +220,8 @@ def test_gemm_plan_of_the_wide_projections(W):
         (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),
         (343, 6144, 4096): (1, 12, 4), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),
         (370, 10240, 8192): (1, 12, 2), (370, 8192, 28672): (1, 12, 4),
-        (476, 16384, 512): (2, 8, 1), (680, 16384, 512): (3, 8, 1),
+        (476, 16384, 512): (2, 8, 2), (680, 16384, 512): (3, 8, 1), (680, 6144, 4096): (2, 12, 2),
+        (680, 4096, 14336): (2, 12, 4), (512, 4096, 4096): (2, 8, 4),
         (1237, 4096, 14336): (5, 8, 1), (1237, 128256, 4096): (5, 8, 1),
     }
     for (M, N, K), (rb, mt, splits) in tiles.items():
