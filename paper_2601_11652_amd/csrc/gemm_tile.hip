@@ -278,21 +278,24 @@ static void launch_tile(const uint16_t *A, const uint16_t *W, float *C, int M, i
 }
 
 // Tile shapes (measured at 7-1237 rows of the 8B and 70B projections, cold weights):
-// 8 waves in 2 x 4 or 4 x 2 wave tiles of 3 x 1, 3 x 2 or 2 x 2 fragments, two waves per
-// SIMD; the wider the column tile, the fewer times the activation slice is re-read.  At
+// 8 waves in 2 x 4 or 4 x 2 wave tiles of 3 x 1, 3 x 2, 2 x 2 or 4 x 2 fragments, two waves
+// per SIMD; the wider the column tile, the fewer times the activation slice is re-read.  At
 // 33-128 rows 64 x 128 and 128 x 128 tiles of single-fragment wave tiles; at most 32 rows
 // a 32 x 256 tile of 4 waves with a deep K split.  At these row counts the activation slice
 // and the fp32 partials are small next to the weights, so the loads are almost all weights.
+// The 384 x 128 and 256 x 256 tiles stage one K step per chunk in a ring of 6 (at 300-1237
+// rows 0-9% faster than two K steps in a ring of 4, which holds more K in flight: with
+// half-size chunks each barrier waits on less).
 TileShape tile_shape(int variant) {
   switch (variant) {
     case 1: return {192, 128, 4};
     case 4: return {192, 256, 4};
-    case 12: return {384, 128, 2};
+    case 12: return {384, 128, 1};
     case 13: return {256, 128, 2};
     case 5: return {32, 256, 4};
     case 6: return {64, 128, 4};
     case 7: return {128, 128, 4};
-    case 17: return {256, 256, 2};
+    case 17: return {256, 256, 1};
   }
   return {0, 0, 0};
 }
@@ -302,12 +305,12 @@ void gemm_bf16_tile(const uint16_t *A, const uint16_t *W, float *C, int M, int N
   switch (variant) {
     case 1: launch_tile<2, 4, 3, 1, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
     case 4: launch_tile<2, 4, 3, 2, 4, 2>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
-    case 12: launch_tile<4, 2, 3, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 12: launch_tile<4, 2, 3, 2, 1, 6>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
     case 13: launch_tile<4, 2, 2, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
     case 5: launch_tile<1, 4, 1, 2, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;   // 4 waves
     case 6: launch_tile<2, 4, 1, 1, 4, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
     case 7: launch_tile<4, 2, 1, 2, 4, 3>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
-    case 17: launch_tile<2, 4, 4, 2, 2, 4>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
+    case 17: launch_tile<2, 4, 4, 2, 1, 6>(A, W, C, M, N, K, ldc, rm, s, kc_split, sw); break;
   }
 }
 
