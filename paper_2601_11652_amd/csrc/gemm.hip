@@ -233,9 +233,12 @@ static constexpr int kPairedWavesMinMT = 5;
 //     6-13 % faster than 256 x 128 at 512-1237 rows), else 384- or 256-row tiles of 128
 //     columns, whichever pads fewer rows (at 680 rows 384-row tiles: QKV 66 -> 51 us, down
 //     117 -> 99).
-// K is split in powers of two while the work items fit one round of 256 workgroups and
-// each split keeps at least 8 chunks (fewer splits cost the GEMMs more than the row
-// kernels save).  The ring holds all rows of a row block of at most 256 rows: 64-column
+// K is split into as many ranges as the work items fit one round of 256 workgroups (at
+// most 8, 16 for the 32-row tile), each range keeping at least 8 chunks: not only powers
+// of two, since a round that leaves CUs idle costs the GEMM more than the row kernels save
+// on fewer partials (QKV of 80 tiles on 3 ranges: 70B at 370 rows 92 -> 72 us alone, the
+// 70B step 76.9 -> 75.8 ms; QKV of 48 tiles on 5: 8B at 100 rows 16.5 -> 14.9 us alone, the
+// 8B step at 171 rows unchanged, the extra partial costing the row kernels what it saves).  The ring holds all rows of a row block of at most 256 rows: 64-column
 // wave tiles for wide outputs, 32-column tiles with a deeper ring otherwise (8 waves per
 // workgroup from kPairedWavesMinMT row fragments on); K split for one resident round.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
@@ -259,8 +262,8 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
       const int tiles = ((mf * 32 + ts.bm - 1) / ts.bm) * ((N + ts.bn - 1) / ts.bn);
       const int KC = K / (16 * ts.ks);
       const int s_max = variant == 5 ? 16 : 8;
-      int s = 1;
-      while (s < s_max && tiles * s * 2 <= 256 && KC / (s * 2) >= 8) s *= 2;
+      int s = std::max(1, std::min(s_max, 256 / tiles));
+      while (s > 1 && KC / s < 8) --s;
       const int kcs = (KC + s - 1) / s;
       c.kind = 4;
       c.variant = variant;

@@ -199,8 +199,9 @@ def test_gemm_plan_of_the_wide_projections(W):
     faster: the output projection at <= 32 rows, the LM head (>= 65536 columns) at 33-160
     rows, outputs of >= 16384 columns at 129-160 rows (64-column wave tiles, gate/up of the
     wide test model with two K ranges), small projections at <= 32 rows.  Elsewhere the
-    LDS-staged tiles (variant 4) with K split in powers of two while the work items fit one
-    round of 256 workgroups and each split keeps >= 8 chunks (up to 16 at <= 32 rows);
+    LDS-staged tiles (variant 4) with K split into as many ranges as the work items fit one
+    round of 256 workgroups, at most 8 (16 at <= 32 rows), each keeping >= 8 chunks (5
+    ranges for 48 tiles, 3 for 80);
     beyond 384 rows 256 x 256 tiles for outputs of >= 16384 columns, else the 384- or
     256-row tiles, whichever pads fewer rows."""
     ring = {  # (M, N, K): kind
@@ -213,13 +214,13 @@ def test_gemm_plan_of_the_wide_projections(W):
     tiles = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
         (7, 6144, 4096): (1, 1, 8), (32, 28672, 4096): (1, 1, 2), (7, 4096, 14336): (1, 1, 16),
         (7, 128256, 4096): (1, 1, 1),
-        (44, 16384, 512): (1, 2, 1), (41, 6144, 4096): (1, 2, 4), (64, 4096, 4096): (1, 2, 8),
+        (44, 16384, 512): (1, 2, 1), (41, 6144, 4096): (1, 2, 5), (64, 4096, 4096): (1, 2, 8),
         (87, 28672, 4096): (1, 4, 1), (128, 4096, 14336): (1, 4, 8),
-        (150, 6144, 4096): (1, 6, 4), (150, 4096, 14336): (1, 6, 8),
-        (171, 6144, 4096): (1, 6, 4), (171, 4096, 4096): (1, 6, 8), (171, 28672, 4096): (1, 6, 1),
+        (150, 6144, 4096): (1, 6, 5), (150, 4096, 14336): (1, 6, 8),
+        (171, 6144, 4096): (1, 6, 5), (171, 4096, 4096): (1, 6, 8), (171, 28672, 4096): (1, 6, 1),
         (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),
-        (343, 6144, 4096): (1, 12, 4), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),
-        (370, 10240, 8192): (1, 12, 2), (370, 8192, 28672): (1, 12, 4),
+        (343, 6144, 4096): (1, 12, 5), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),
+        (370, 10240, 8192): (1, 12, 3), (370, 8192, 28672): (1, 12, 4),
         (476, 16384, 512): (2, 8, 2), (680, 16384, 512): (3, 8, 1), (680, 6144, 4096): (2, 12, 2),
         (680, 4096, 14336): (2, 12, 4), (512, 4096, 4096): (2, 8, 4),
         (1237, 4096, 14336): (5, 8, 1), (1237, 128256, 4096): (5, 8, 1),
