@@ -228,11 +228,14 @@ static constexpr int kPairedWavesMinMT = 5;
 //   6: 192-row tiles, 256 columns wide only for the LM head (measured over whole steps: for
 //     gate/up the 128-column tile in one K range costs the same and halves the partial sums
 //     the SwiGLU kernel reads);
-//   7-8: one 256-row tile, 9-12: one 384-row tile;
-//   beyond (> 384 rows): 256 x 256 tiles for outputs of >= 16384 columns (gate/up, LM head:
-//     6-13 % faster than 256 x 128 at 512-1237 rows), else 384- or 256-row tiles of 128
-//     columns, whichever pads fewer rows (at 680 rows 384-row tiles: QKV 66 -> 51 us, down
-//     117 -> 99).
+//   7-8: one 256-row tile, 256 columns wide for the LM head (at 240 rows 374 -> 325 us);
+//     at 128 columns for the rest (gate/up keeps one K range and its SwiGLU epilogue);
+//   9-12: one 384-row tile (at 343-370 rows 10-25 % faster than two 256-row tiles);
+//   beyond (> 384 rows): 256 x 256 tiles with the K split below (at 476-1237 rows 9-30 %
+//     off QKV + O + down per layer against 384- or 256-row tiles of 128 columns: 8B at
+//     1237 rows 371 -> 259 us, 70B at 476 rows 512 -> 380 us; in the 8B step at 1237 rows
+//     the projections 21.9 -> 19.3 ms, the row kernels reading the added partials
+//     1.87 -> 2.61 ms, the step 45.5 -> 44.2 ms).
 // K is split into as many ranges as the work items fit one round of 256 workgroups (at
 // most 8, 16 for the 32-row tile), each range keeping at least 8 chunks: not only powers
 // of two, since a round that leaves CUs idle costs the GEMM more than the row kernels save
@@ -252,10 +255,9 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   else if (mf <= 4) variant = lm_wide ? 0 : 7;
   else if (mf == 5) variant = N < 16384 ? 1 : 0;
   else if (mf == 6) variant = lm_wide ? 4 : 1;
-  else if (mf <= 8) variant = 13;
+  else if (mf <= 8) variant = lm_wide ? 17 : 13;
   else if (mf <= 12) variant = 12;
-  else if (N >= 16384) variant = 17;
-  else variant = (mf + 11) / 12 * 12 <= (mf + 7) / 8 * 8 ? 12 : 13;   // the tile that pads fewer rows
+  else variant = 17;
   if (variant) {
     const TileShape ts = tile_shape(variant);
     if (K % (16 * ts.ks) == 0) {

@@ -202,8 +202,8 @@ def test_gemm_plan_of_the_wide_projections(W):
     LDS-staged tiles (variant 4) with K split into as many ranges as the work items fit one
     round of 256 workgroups, at most 8 (16 at <= 32 rows), each keeping >= 8 chunks (5
     ranges for 48 tiles, 3 for 80);
-    beyond 384 rows 256 x 256 tiles for outputs of >= 16384 columns, else the 384- or
-    256-row tiles, whichever pads fewer rows."""
+    225-256 rows one 256-row tile, 256 columns wide for the LM head; beyond 384 rows
+    256 x 256 tiles for every projection."""
     ring = {  # (M, N, K): kind
         (7, 4096, 4096): 1, (7, 1024, 256): 1, (44, 128256, 4096): 2, (150, 128256, 4096): 2,
         (150, 28672, 4096): 2, (150, 16384, 512): 2, (150, 32768, 512): 2,
@@ -221,9 +221,10 @@ def test_gemm_plan_of_the_wide_projections(W):
         (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),
         (343, 6144, 4096): (1, 12, 5), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),
         (370, 10240, 8192): (1, 12, 3), (370, 8192, 28672): (1, 12, 4),
-        (476, 16384, 512): (2, 8, 2), (680, 16384, 512): (3, 8, 1), (680, 6144, 4096): (2, 12, 2),
-        (680, 4096, 14336): (2, 12, 4), (512, 4096, 4096): (2, 8, 4),
-        (1237, 4096, 14336): (5, 8, 1), (1237, 128256, 4096): (5, 8, 1),
+        (476, 16384, 512): (2, 8, 2), (680, 16384, 512): (3, 8, 1), (680, 6144, 4096): (3, 8, 3),
+        (680, 4096, 14336): (3, 8, 5), (512, 4096, 4096): (2, 8, 8),
+        (1237, 4096, 14336): (5, 8, 3), (1237, 128256, 4096): (5, 8, 1), (1237, 6144, 4096): (5, 8, 2),
+        (240, 128256, 4096): (1, 8, 1), (240, 28672, 4096): (1, 8, 1), (2108, 1024, 256): (9, 8, 2),
     }
     for (M, N, K), (rb, mt, splits) in tiles.items():
         t = W.gemm_plan(M, N, K)

@@ -7,8 +7,8 @@
   max-abs);
 * a batch of plain-decode requests only (no draft rows; the draft distributions may be
   NULL);
-* more than 256 rows (24 requests x 17 rows = 408), which the weight-ring GEMMs serve in
-  two row blocks, and 2108 rows (124 x 17), which run the LDS-staged tile GEMM;
+* more than 256 rows (24 requests x 17 rows = 408) and 2108 rows (124 x 17), which the
+  LDS-staged tile GEMM serves in two and nine rows of 256 x 256 tiles;
 * 129-256 rows, where the 32-column weight-ring GEMM runs 8 waves on two row halves: an
   odd number of 32-row fragments (150 rows: one half carries a zero fragment) and an even
   one (192 rows);
@@ -17,7 +17,7 @@
 * a bf16 model of odd widths: d_model 96, d_ff 160, 3 query heads on 1 kv head, vocabulary
   1056.  Every projection then has a partly filled last column tile and a K shorter than
   one weight ring, and the GQA group is not a power of two; at 34 rows (weight ring) and
-  612 rows (tile GEMM).
+  612 rows (256 x 256 tiles, most columns of the narrow projections past the edge).
 """
 import numpy as np
 import pytest
@@ -118,7 +118,8 @@ def test_plain_decode_batch_without_draft_rows(shape, check):
 
 
 def test_more_than_256_rows_in_two_row_tiles():
-    """408 rows: two 256-row tiles of the LDS-staged GEMM, the second one mostly padding."""
+    """408 rows: two rows of 256 x 256 tiles of the LDS-staged GEMM, the second mostly
+    padding, with K split."""
     B = 24
     ctx = [int(c) for c in np.random.default_rng(5).integers(0, 96, size=B)]
     _run_case(MINI_BF16, ctx, [16] * B, _bf16_abs)

@@ -7,9 +7,8 @@ columns), vocabulary 32768, bf16, 2 layers.
 
 Cases: 44 rows (every projection on 64 x 128 tiles), 153 rows (gate/up and the LM head on
 the 64-column weight ring, gate/up with two K ranges summed in fixed order; the others on
-192-row tiles), 476 and 680 rows (gate/up and the LM head on 256 x 256 tiles, gate/up with
-two K ranges at 476 rows and with SwiGLU in its epilogue at 680; the others on 256-row
-tiles).  Checks: logits within 2e-2 max-abs of the oracle, every written K/V value within
+192-row tiles), 476 and 680 rows (every projection on 256 x 256 tiles, gate/up with two K
+ranges at 476 rows and with SwiGLU in its epilogue at 680, the narrow ones with K split).  Checks: logits within 2e-2 max-abs of the oracle, every written K/V value within
 max(two bf16 ulps at its head vector's scale, twice the oracle's floor of its layer),
 untouched slots bit-identical, decisions on the GPU's own logits bit-exact except flagged
 near-ties.
