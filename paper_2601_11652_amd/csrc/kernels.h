@@ -109,7 +109,7 @@ constexpr int kAttnCombineChunks = 8;  // chunks the combine loads per round of 
 void attention_bf16_main(const StepDesc &d, const AttnItem *items, int n_items, const uint16_t *q,
                          const uint16_t *k_pool, const uint16_t *v_pool, float *part_o, float *part_ml,
                          int nq, int nkv, int hd, hipStream_t s);
-void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_groups,
+void attention_bf16_combine(const StepDesc &d, const AttnGroup *groups, int n_groups, int max_group_chunks,
                             const float *part_o, const float *part_ml, uint16_t *out, bool out_packed,
                             int out_K, int nq, int nkv, int hd, hipStream_t s);
 void attention_f32(const StepDesc &d, int B, const float *q, const float *k_pool,

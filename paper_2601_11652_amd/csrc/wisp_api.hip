@@ -57,6 +57,7 @@ struct Plan {
          w_part = 0, w_attn_o = 0, w_attn_ml = 0, w_sm = 0, w_si = 0, w_ss = 0, w_rk = 0, w_ri = 0,
          w_rR = 0, w_vtok = 0, w_lmm = 0, w_lmi = 0, total = 0;
   int lm_tiles = 0;                  // output tiles of the LM head (bf16): its row-maxima columns
+  int max_group_chunks = 0;          // most chunks any attention group combines
 };
 
 
@@ -246,6 +247,7 @@ wisp_status make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bo
               p.items.push_back(it);
             }
             gr.n_items = (int32_t)p.items.size() - gr.first_item;
+            p.max_group_chunks = std::max(p.max_group_chunks, (int)gr.n_items);
             p.groups.push_back(gr);
           }
       }
@@ -555,7 +557,7 @@ wisp_status run_forward(const Plan &p, const wisp_model *m, const wisp_kv *kv, c
                             (const uint16_t *)vl, po, pml, p.nq, p.nkv, p.hd, s);
       }
       ProfScope ps(WISP_PROF_ATTN_COMBINE, 0, 0, s);
-      attention_bf16_combine(sd, groups, (int)p.groups.size(), po, pml, (uint16_t *)ao, true, p.qdim, p.nq,
+      attention_bf16_combine(sd, groups, (int)p.groups.size(), p.max_group_chunks, po, pml, (uint16_t *)ao, true, p.qdim, p.nq,
                              p.nkv, p.hd, s);
     } else {
       ProfScope ps(WISP_PROF_ATTN, attn_bytes, attn_flops, s);
@@ -900,7 +902,7 @@ wisp_status wisp_attention(const wisp_model *model, const wisp_kv *kv, const wis
       float *pml = reinterpret_cast<float *>(ws + p.w_attn_ml);
       attention_bf16_main(sd, items, (int)p.items.size(), (const uint16_t *)q, (const uint16_t *)kv->k_pool,
                           (const uint16_t *)kv->v_pool, po, pml, p.nq, p.nkv, p.hd, s);
-      attention_bf16_combine(sd, groups, (int)p.groups.size(), po, pml, (uint16_t *)out, false, p.qdim, p.nq,
+      attention_bf16_combine(sd, groups, (int)p.groups.size(), p.max_group_chunks, po, pml, (uint16_t *)out, false, p.qdim, p.nq,
                              p.nkv, p.hd, s);
     } else {
       attention_f32(sd, p.B, (const float *)q, (const float *)kv->k_pool, (const float *)kv->v_pool,
