@@ -212,18 +212,20 @@ wisp_status make_plan(Plan &p, const wisp_model *m, const wisp_batch_desc *d, bo
       while (rounds * slots < fewest) ++rounds;
       int L = 2;
       while (L < L_max && count_items(L) > rounds * slots) ++L;
-      // Small batches leave most wave slots idle even at the shortest items, and their step
-      // is latency-bound: longer items then cost little, while every further 8 chunks of a
-      // group cost the combine another round of dependent loads.  Below half the slots,
-      // items grow until no group has more than kAttnCombineChunks of them (measured at
-      // B = 1: attention + combine 10.4 + 13.9 us per layer at 21 chunks per group).
-      if (count_items(L) * 2 <= slots) {
+      // Small batches leave wave slots idle even at the shortest items, and their step is
+      // latency-bound: longer items then cost little, while a group of more than
+      // kAttnCombineChunks chunks costs the combine further dependent loads.  Whenever the
+      // items still fit one round of the wave slots, they grow until no group has more
+      // than kAttnCombineChunks of them (B = 1: attention + combine 10.4 + 13.9 -> 14.3 +
+      // 4.2 us per layer; B = 16: 27.7 -> 25.5 us; B = 4 and 8 within 3 %).
+      {
         int64_t most = 0;
         for (int i = 0; i < p.B; ++i) {
           const int nrbg = (nrow[i] * p.G + kAttnRowsPerItem - 1) / kAttnRowsPerItem;
           for (int g = 0; g < nrbg; ++g) most = std::max<int64_t>(most, (group_tokens(i, g) + 31) / 32);
         }
-        L = (int)std::min<int64_t>(L_max, std::max<int64_t>(L, (most + kAttnCombineChunks - 1) / kAttnCombineChunks));
+        const int Lc = (int)std::min<int64_t>(L_max, std::max<int64_t>(L, (most + kAttnCombineChunks - 1) / kAttnCombineChunks));
+        if (count_items(Lc) <= slots) L = Lc;
       }
       for (int i = 0; i < p.B; ++i) {
         const int rows = nrow[i] * p.G;
