@@ -219,8 +219,11 @@ static constexpr int kPairedWavesMinMT = 5;
 // (above) where it streams faster or K does not fit the tile's chunk.  Tile variant by
 // row fragments, measured with cold weights on the 8B and 70B projections at 7-1237 rows:
 //   1 (<= 32 rows): the 32 x 256 tile with up to 16 K splits for projections of >= 20M
-//     weights (at 7 rows QKV 13.4 -> 11.5 us, gate/up 44.0 -> 39.4, down 24.0 -> 20.1, LM
-//     head 169.5 -> 158.9); the output projection streams as fast on the ring;
+//     weights (at 7 rows QKV 13.4 -> 11.5 us, down 24.0 -> 20.1, LM head 169.5 -> 158.9);
+//     the output projection streams as fast on the ring; outputs of 16384-32768 columns
+//     (the 8B gate/up) take 64 x 128 tiles in one K range, which fill as many CUs as the
+//     32-row tile with two (at 7-23 rows 36-39 us against 38-40) and keep the SwiGLU
+//     epilogue (8B steps at B = 1, 2, 4: 4.05 -> 3.84, 4.12 -> 3.90, 4.38 -> 4.12 ms);
 //   2: 64 x 128 tiles, 3-4: 128 x 128 (10-23 % faster than the ring on QKV, O, gate/up
 //     and down); the LM head stays on the ring;
 //   5: the 192-row tile below 16384 columns (QKV 22.1 -> 19.5 us, down 38.4 -> 32.4); the
@@ -250,7 +253,7 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   const int KF = K / 16;
   const bool lm_wide = N >= 65536;
   int variant;
-  if (mf == 1) variant = (int64_t)N * K >= ((int64_t)20 << 20) ? 5 : 0;
+  if (mf == 1) variant = N >= 16384 && N <= 32768 ? 6 : (int64_t)N * K >= ((int64_t)20 << 20) ? 5 : 0;
   else if (mf == 2) variant = lm_wide ? 0 : 6;
   else if (mf <= 4) variant = lm_wide ? 0 : 7;
   else if (mf == 5) variant = N < 16384 ? 1 : 0;

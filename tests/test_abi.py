@@ -212,7 +212,7 @@ def test_gemm_plan_of_the_wide_projections(W):
         assert W.gemm_plan(M, N, K)["kind"] == kind, (M, N, K, W.gemm_plan(M, N, K))
     assert W.gemm_plan(150, 16384, 512)["splits"] == 2
     tiles = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
-        (7, 6144, 4096): (1, 1, 8), (32, 28672, 4096): (1, 1, 2), (7, 4096, 14336): (1, 1, 16),
+        (7, 6144, 4096): (1, 1, 8), (32, 28672, 4096): (1, 2, 1), (7, 57344, 8192): (1, 1, 1), (7, 4096, 14336): (1, 1, 16),
         (7, 128256, 4096): (1, 1, 1),
         (44, 16384, 512): (1, 2, 1), (41, 6144, 4096): (1, 2, 5), (64, 4096, 4096): (1, 2, 8),
         (87, 28672, 4096): (1, 4, 1), (128, 4096, 14336): (1, 4, 8),

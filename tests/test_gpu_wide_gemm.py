@@ -5,7 +5,9 @@ small test models never had.  This model makes both wide at a width the oracle r
 in seconds: d_model 512, 8 query heads on 2 kv heads of 64, d_ff 8192 (gate/up 16384
 columns), vocabulary 32768, bf16, 2 layers.
 
-Cases: 44 rows (every projection on 64 x 128 tiles), 153 rows (gate/up and the LM head on
+Cases: 14 rows (gate/up and the LM head on 64 x 128 tiles in one K range, with their
+SwiGLU and row-maxima epilogues; the narrower projections on the weight ring), 44 rows
+(every projection on 64 x 128 tiles), 153 rows (gate/up and the LM head on
 the 64-column weight ring, gate/up with two K ranges summed in fixed order; the others on
 192-row tiles), 476 and 680 rows (every projection on 256 x 256 tiles, gate/up with two K
 ranges at 476 rows and with SwiGLU in its epilogue at 680, the narrow ones with K split).  Checks: logits within 2e-2 max-abs of the oracle, every written K/V value within
@@ -26,12 +28,13 @@ WIDE_BF16 = wi.ModelShape("wide-bf16", 2, 512, 8, 2, 64, 8192, 32768, "bf16", 10
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("B", [8, 9, 28, 40], ids=["44rows", "153rows", "476rows", "680rows"])
+@pytest.mark.parametrize("B", [3, 8, 9, 28, 40], ids=["14rows", "44rows", "153rows", "476rows", "680rows"])
 def test_wide_projections_match_the_oracle(B):
     r = np.random.default_rng(8192 + B)
     ctx = r.integers(0, 64, size=B).astype(np.int32)
-    # 8 requests of 36 drafts in all: 44 rows; otherwise B requests of 16 drafts: 17 B rows
-    gamma = np.array([7, 1, 5, 3, 6, 4, 2, 8] if B == 8 else [16] * B, np.int32)
+    # 3 requests of 11 drafts: 14 rows; 8 requests of 36 drafts in all: 44 rows; otherwise
+    # B requests of 16 drafts: 17 B rows
+    gamma = np.array({3: [6, 1, 4], 8: [7, 1, 5, 3, 6, 4, 2, 8]}.get(B, [16] * B), np.int32)
     mix = wi.custom_mix(WIDE_BF16, ctx, gamma, kv_source="prefill", name=f"wide-{B}", t_draft=1.0,
                         sigma=0.5)
     log(f"{WIDE_BF16.name}: B={B} M={mix.M} ctx={ctx.tolist()} gamma={gamma.tolist()}")
