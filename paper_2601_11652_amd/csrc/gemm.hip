@@ -226,8 +226,10 @@ static constexpr int kPairedWavesMinMT = 5;
 //     epilogue (8B steps at B = 1, 2, 4: 4.05 -> 3.84, 4.12 -> 3.90, 4.38 -> 4.12 ms);
 //   2: 64 x 128 tiles, 3-4: 128 x 128 (10-23 % faster than the ring on QKV, O, gate/up
 //     and down); the LM head stays on the ring;
-//   5: the 192-row tile below 16384 columns (QKV 22.1 -> 19.5 us, down 38.4 -> 32.4); the
-//     ring for gate/up and the LM head;
+//   5: the 192-row tile (QKV 22.1 -> 19.5 us, down 38.4 -> 32.4; gate/up in one K range
+//     as fast as the ring with two, 59.0 against 60.5 us, and with the SwiGLU epilogue:
+//     8B steps at B = 26 / 28 6.89 / 6.93 -> 6.74 / 6.79 ms);
+//     the ring for the LM head;
 //   6: 192-row tiles, 256 columns wide only for the LM head (measured over whole steps: for
 //     gate/up the 128-column tile in one K range costs the same and halves the partial sums
 //     the SwiGLU kernel reads);
@@ -256,7 +258,7 @@ GemmCfg gemm_bf16_plan(int M, int N, int K) {
   if (mf == 1) variant = N >= 16384 && N <= 32768 ? 6 : (int64_t)N * K >= ((int64_t)20 << 20) ? 5 : 0;
   else if (mf == 2) variant = lm_wide ? 0 : 6;
   else if (mf <= 4) variant = lm_wide ? 0 : 7;
-  else if (mf == 5) variant = N < 16384 ? 1 : 0;
+  else if (mf == 5) variant = lm_wide ? 0 : 1;
   else if (mf == 6) variant = lm_wide ? 4 : 1;
   else if (mf <= 8) variant = lm_wide ? 17 : 13;
   else if (mf <= 12) variant = 12;

@@ -197,26 +197,26 @@ def test_binding_rejects_host_and_mistyped_tensors(W):
 def test_gemm_plan_of_the_wide_projections(W):
     """The launch plan by row fragments (32 rows each).  The weight ring where it streams
     faster: the output projection at <= 32 rows, the LM head (>= 65536 columns) at 33-160
-    rows, outputs of >= 16384 columns at 129-160 rows (64-column wave tiles, gate/up of the
-    wide test model with two K ranges), small projections at <= 32 rows.  Elsewhere the
-    LDS-staged tiles (variant 4) with K split into as many ranges as the work items fit one
-    round of 256 workgroups, at most 8 (16 at <= 32 rows), each keeping >= 8 chunks (5
-    ranges for 48 tiles, 3 for 80);
-    225-256 rows one 256-row tile, 256 columns wide for the LM head; beyond 384 rows
-    256 x 256 tiles for every projection."""
+    rows (64-column wave tiles), small projections at <= 32 rows.  Elsewhere the LDS-staged
+    tiles (variant 4) with K split into as many ranges as the work items fit one round of
+    256 workgroups, at most 8 (16 at <= 32 rows), each keeping >= 8 chunks (5 ranges for 48
+    tiles, 3 for 80); at <= 32 rows outputs of 16384-32768 columns on 64-row tiles in one K
+    range; 129-160 rows gate/up on the 192-row tile in one K range; 225-256 rows one 256-row
+    tile, 256 columns wide for the LM head; beyond 384 rows 256 x 256 tiles for every
+    projection."""
     ring = {  # (M, N, K): kind
         (7, 4096, 4096): 1, (7, 1024, 256): 1, (44, 128256, 4096): 2, (150, 128256, 4096): 2,
-        (150, 28672, 4096): 2, (150, 16384, 512): 2, (150, 32768, 512): 2,
+        (44, 65536, 512): 2, (153, 65536, 512): 2,
     }
     for (M, N, K), kind in ring.items():
         assert W.gemm_plan(M, N, K)["kind"] == kind, (M, N, K, W.gemm_plan(M, N, K))
-    assert W.gemm_plan(150, 16384, 512)["splits"] == 2
     tiles = {  # (M, N, K): (row tiles, fragments per row tile, K ranges)
         (7, 6144, 4096): (1, 1, 8), (32, 28672, 4096): (1, 2, 1), (7, 57344, 8192): (1, 1, 1), (7, 4096, 14336): (1, 1, 16),
         (7, 128256, 4096): (1, 1, 1),
         (44, 16384, 512): (1, 2, 1), (41, 6144, 4096): (1, 2, 5), (64, 4096, 4096): (1, 2, 8),
         (87, 28672, 4096): (1, 4, 1), (128, 4096, 14336): (1, 4, 8),
         (150, 6144, 4096): (1, 6, 5), (150, 4096, 14336): (1, 6, 8),
+        (150, 28672, 4096): (1, 6, 1), (153, 16384, 512): (1, 6, 1),
         (171, 6144, 4096): (1, 6, 5), (171, 4096, 4096): (1, 6, 8), (171, 28672, 4096): (1, 6, 1),
         (171, 4096, 14336): (1, 6, 8), (171, 128256, 4096): (1, 6, 1),
         (343, 6144, 4096): (1, 12, 5), (343, 4096, 14336): (1, 12, 8), (343, 28672, 4096): (1, 12, 1),

@@ -3,14 +3,15 @@
 The 8B / 70B shapes have gate/up and LM-head outputs of at least 16384 columns, which the
 small test models never had.  This model makes both wide at a width the oracle recomputes
 in seconds: d_model 512, 8 query heads on 2 kv heads of 64, d_ff 8192 (gate/up 16384
-columns), vocabulary 32768, bf16, 2 layers.
+columns), vocabulary 65536 (wide enough for the LM head's own plan), bf16, 2 layers.
 
-Cases: 14 rows (gate/up and the LM head on 64 x 128 tiles in one K range, with their
-SwiGLU and row-maxima epilogues; the narrower projections on the weight ring), 44 rows
-(every projection on 64 x 128 tiles), 153 rows (gate/up and the LM head on
-the 64-column weight ring, gate/up with two K ranges summed in fixed order; the others on
-192-row tiles), 476 and 680 rows (every projection on 256 x 256 tiles, gate/up with two K
-ranges at 476 rows and with SwiGLU in its epilogue at 680, the narrow ones with K split).  Checks: logits within 2e-2 max-abs of the oracle, every written K/V value within
+Cases: 14 rows (gate/up on 64 x 128 tiles in one K range with the SwiGLU epilogue, the LM
+head on 32 x 256 tiles with the row-maxima epilogue, the narrower projections on the
+weight ring), 44 rows (the LM head on the 64-column weight ring, the rest on 64 x 128
+tiles), 153 rows (the LM head on the 64-column weight ring, the rest on 192-row tiles,
+gate/up in one K range with SwiGLU in its epilogue), 476 and 680 rows (every projection on
+256 x 256 tiles, gate/up with two K ranges at 476 rows and with SwiGLU in its epilogue at
+680, the narrow ones with K split).  Checks: logits within 2e-2 max-abs of the oracle, every written K/V value within
 max(two bf16 ulps at its head vector's scale, twice the oracle's floor of its layer),
 untouched slots bit-identical, decisions on the GPU's own logits bit-exact except flagged
 near-ties.
@@ -24,7 +25,7 @@ from gpu_harness import Workload, check_decisions_on_gpu_logits, check_written, 
 
 pytestmark = pytest.mark.gpu
 
-WIDE_BF16 = wi.ModelShape("wide-bf16", 2, 512, 8, 2, 64, 8192, 32768, "bf16", 10000.0)
+WIDE_BF16 = wi.ModelShape("wide-bf16", 2, 512, 8, 2, 64, 8192, 65536, "bf16", 10000.0)
 
 
 @pytest.mark.timeout(600)
