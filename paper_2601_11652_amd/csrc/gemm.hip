@@ -225,14 +225,15 @@ static constexpr int kPairedWavesMinMT = 5;
 //     32-row tile with two (at 7-23 rows 36-39 us against 38-40) and keep the SwiGLU
 //     epilogue (8B steps at B = 1, 2, 4: 4.05 -> 3.84, 4.12 -> 3.90, 4.38 -> 4.12 ms);
 //   2: 64 x 128 tiles, 3-4: 128 x 128 (10-23 % faster than the ring on QKV, O, gate/up
-//     and down); the LM head stays on the ring;
+//     and down); the LM head stays on the ring (the tiles 7-44 % slower for it at 41-150
+//     rows);
 //   5: the 192-row tile (QKV 22.1 -> 19.5 us, down 38.4 -> 32.4; gate/up in one K range
 //     as fast as the ring with two, 59.0 against 60.5 us, and with the SwiGLU epilogue:
 //     8B steps at B = 26 / 28 6.89 / 6.93 -> 6.74 / 6.79 ms);
 //     the ring for the LM head;
 //   6: 192-row tiles, 256 columns wide only for the LM head (measured over whole steps: for
-//     gate/up the 128-column tile in one K range costs the same and halves the partial sums
-//     the SwiGLU kernel reads);
+//     gate/up the 128-column tile in one K range, with the SwiGLU epilogue, beats the
+//     256-column one, which needs two K ranges to fill the CUs);
 //   7-8: one 256-row tile, 256 columns wide for the LM head (at 240 rows 374 -> 325 us);
 //     at 128 columns for the rest (gate/up keeps one K range and its SwiGLU epilogue);
 //   9-12: one 384-row tile (at 343-370 rows 10-25 % faster than two 256-row tiles);
@@ -246,9 +247,10 @@ static constexpr int kPairedWavesMinMT = 5;
 // of two, since a round that leaves CUs idle costs the GEMM more than the row kernels save
 // on fewer partials (QKV of 80 tiles on 3 ranges: 70B at 370 rows 92 -> 72 us alone, the
 // 70B step 76.9 -> 75.8 ms; QKV of 48 tiles on 5: 8B at 100 rows 16.5 -> 14.9 us alone, the
-// 8B step at 171 rows unchanged, the extra partial costing the row kernels what it saves).  The ring holds all rows of a row block of at most 256 rows: 64-column
-// wave tiles for wide outputs, 32-column tiles with a deeper ring otherwise (8 waves per
-// workgroup from kPairedWavesMinMT row fragments on); K split for one resident round.
+// 8B step at 171 rows unchanged, the extra partial costing the row kernels what it saves).
+// The ring holds all rows of a row block of at most 256 rows: 64-column wave tiles for
+// wide outputs, 32-column tiles with a deeper ring otherwise (8 waves per workgroup from
+// kPairedWavesMinMT row fragments on); K split for one resident round.
 GemmCfg gemm_bf16_plan(int M, int N, int K) {
   GemmCfg c{};
   const int mf = (M + 31) / 32;
